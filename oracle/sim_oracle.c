@@ -1,0 +1,165 @@
+/*
+ * ORACLE -- test infrastructure only.  Nothing in the product path may link,
+ * load or call this file; only tests, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no code, header or constant generator with
+ * the GPU simulator.
+ *
+ * A plain, slow, single-threaded CPU simulator of AlpaServe's serving model,
+ * written from the paper's definitions:
+ *   - Sec. 4.3 (runtime scheduling): a central controller sends each request
+ *     to the group with the shortest queue among the groups that host the
+ *     requested model; every group runs one first-come-first-served queue and
+ *     rejects a request it cannot finish within the SLO, which is possible
+ *     because execution times are predictable.
+ *   - Sec. 3.2 (SLO experiment): requests that would miss the deadline even if
+ *     scheduled immediately are dropped; SLO attainment is the fraction of all
+ *     requests finished within the deadline; the deadline is a multiple
+ *     ("SLO scale") of the model's single-device latency.
+ *   - Sec. 3.4 (queueing analysis): a pipelined group is a chain of stages, each
+ *     a single server; one request's latency is the sum of its stage latencies
+ *     and the throughput is limited by the slowest stage.
+ *   - Sec. 4.2 (placement): a placement partitions the devices into groups,
+ *     each group has one shared parallel configuration (pipeline depth S,
+ *     intra-op degree k) and hosts a subset of the models; a model may be
+ *     replicated on several groups.
+ *
+ * Readings where the paper is silent (each listed in the design notes):
+ *   - "shortest queue" is the group whose stage-0 free time (finish time at
+ *     stage 0 of the last request it accepted; 0 before any) is smallest, ties
+ *     to the lowest group index;
+ *   - the SLO check happens when the request arrives: the projected finish
+ *     f_{S-1} is accepted iff f_{S-1} <= t + slo (a finish exactly at the
+ *     deadline is on time); a rejected request changes no state and is not
+ *     retried on another group;
+ *   - requests of a model that no group hosts are misses (they stay in the
+ *     denominator of the attainment);
+ *   - requests are handled in array order (the trace order breaks ties of
+ *     equal arrival times); slo_m = slo_scale * d_single[m], one fp64 product.
+ *
+ * Per accepted request and stage s of the chosen group g (f_{-1} = t):
+ *     f_s = max(f_{s-1}, F[g][s]) + L[m][c_g][s],   then F[g][s] := f_s.
+ * All arithmetic is IEEE binary64, round to nearest even, no FMA
+ * contraction (build with -ffp-contract=off), no reassociation.
+ *
+ * Verification digest (not part of the paper; it lets a checker compare two
+ * simulators without the full per-request output): accept bits are packed 64
+ * per word (bit i mod 64 of word i div 64), each finished word w folds into
+ * h = (h XOR w) * 0x9E3779B97F4A7C15 mod 2^64 (the last partial word too), and
+ * fin_sum is the sum mod 2^64 of the IEEE bit patterns of accepted finish
+ * times.  Per-request output: finish time if accepted, -1 if rejected, -2 if
+ * no group hosts the model.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_E_ARG (-1)
+#define ORACLE_E_NOMEM (-2)
+
+static double oracle_max(double a, double b) { return a < b ? b : a; }
+
+static uint64_t bits_of(double x) {
+  uint64_t u;
+  memcpy(&u, &x, sizeof u);
+  return u;
+}
+
+/*
+ * Simulate one job: one trace, one placement, one SLO scale.
+ *   t[n], model[n]          trace (seconds; model ids in [0, n_models))
+ *   d_single[n_models]      single-device latency of each model (SLO base)
+ *   cfg_stages[n_configs]   pipeline depth S of each parallel configuration
+ *   stage_lat               [n_models][n_configs][max_stages] stage latencies
+ *   group_cfg[n_groups]     configuration of each group (-1 = unused group)
+ *   host_mask[n_models]     bit g set <=> group g hosts the model
+ *   slo_scale               SLO multiple of d_single
+ * Outputs: *served_out, digest_out[2] = {h, fin_sum}, finish_out[n] (may be NULL).
+ */
+int oracle_simulate_job(int64_t n, const double* t, const int32_t* model, int32_t n_models,
+                        const double* d_single, int32_t n_configs, const int32_t* cfg_stages,
+                        int32_t max_stages, const double* stage_lat, int32_t n_groups,
+                        const int32_t* group_cfg, const uint64_t* host_mask, double slo_scale,
+                        int64_t* served_out, uint64_t* digest_out, double* finish_out) {
+  if (n < 0 || n_models <= 0 || n_configs <= 0 || max_stages <= 0 || n_groups <= 0 ||
+      n_groups > 64 || !served_out || !digest_out)
+    return ORACLE_E_ARG;
+
+  double* F = (double*)calloc((size_t)n_groups * (size_t)max_stages, sizeof(double));
+  double* slo = (double*)malloc((size_t)n_models * sizeof(double));
+  double* f = (double*)malloc((size_t)max_stages * sizeof(double));
+  if (!F || !slo || !f) {
+    free(F);
+    free(slo);
+    free(f);
+    return ORACLE_E_NOMEM;
+  }
+  /* inputs the definitions above do not cover are refused, not guessed */
+  for (int32_t c = 0; c < n_configs; ++c)
+    if (cfg_stages[c] < 1 || cfg_stages[c] > max_stages) goto bad_arg;
+  for (int32_t m = 0; m < n_models; ++m)
+    for (int32_t g = 0; g < 64; ++g)
+      if ((host_mask[m] >> g) & 1u)
+        if (g >= n_groups || group_cfg[g] < 0 || group_cfg[g] >= n_configs) goto bad_arg;
+  for (int64_t i = 0; i < n; ++i)
+    if (model[i] < 0 || model[i] >= n_models) goto bad_arg;
+
+  for (int32_t m = 0; m < n_models; ++m) slo[m] = slo_scale * d_single[m];
+
+  int64_t served = 0;
+  uint64_t h = 0, word = 0, fin_sum = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t m = model[i];
+    const double ti = t[i];
+    const uint64_t mask = host_mask[m];
+    double out;
+    if (mask == 0) {
+      out = -2.0;
+    } else {
+      /* dispatch: least stage-0 free time among hosting groups, lowest index on ties */
+      int32_t gs = -1;
+      for (int32_t g = 0; g < n_groups; ++g) {
+        if (!((mask >> g) & 1u)) continue;
+        if (gs < 0 || F[g * max_stages + 0] < F[gs * max_stages + 0]) gs = g;
+      }
+      const int32_t c = group_cfg[gs];
+      const int32_t S = cfg_stages[c];
+      /* projection through the stage chain */
+      double prev = ti;
+      for (int32_t s = 0; s < S; ++s) {
+        const double lat = stage_lat[((int64_t)m * n_configs + c) * max_stages + s];
+        f[s] = oracle_max(prev, F[gs * max_stages + s]) + lat;
+        prev = f[s];
+      }
+      /* admission */
+      const double deadline = ti + slo[m];
+      if (prev > deadline) {
+        out = -1.0;
+      } else {
+        for (int32_t s = 0; s < S; ++s) F[gs * max_stages + s] = f[s];
+        served += 1;
+        fin_sum += bits_of(prev);
+        word |= (uint64_t)1 << (i & 63);
+        out = prev;
+      }
+    }
+    if (finish_out) finish_out[i] = out;
+    if ((i & 63) == 63 || i == n - 1) {
+      h = (h ^ word) * 0x9E3779B97F4A7C15ULL;
+      word = 0;
+    }
+  }
+  *served_out = served;
+  digest_out[0] = h;
+  digest_out[1] = fin_sum;
+  free(F);
+  free(slo);
+  free(f);
+  return ORACLE_OK;
+
+bad_arg:
+  free(F);
+  free(slo);
+  free(f);
+  return ORACLE_E_ARG;
+}

@@ -1,0 +1,133 @@
+"""Seeded workload generator: determinism, distribution, ordering.
+
+The generator feeds both the oracle and the GPU path, so its output is pinned
+here independently of either: golden SHA-256 of whole traces (regression), and
+statistical checks against the Gamma / Poisson distributions the paper's
+arrival model names (Sec. 3.1 Poisson and Gamma-with-CV arrivals, Sec. 6.2
+Gamma processes parameterised by rate and CV)."""
+import hashlib
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy import stats
+
+from paper_2302_11665_amd.workload import gen, problems
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "gen_hashes.json")
+
+
+def _sha(t, m):
+    h = hashlib.sha256()
+    h.update(np.ascontiguousarray(t, np.float64).tobytes())
+    h.update(np.ascontiguousarray(m, np.int32).tobytes())
+    return h.hexdigest()
+
+
+def golden_traces():
+    """(name, t, model) for the traces whose hashes are committed."""
+    out = []
+    t, m = gen.trace(0, [5.0] * 4, 1.0, 60.0)
+    out.append(("c1_trace", t, m))
+    t, m = gen.trace(2, [4.0] * 16, 3.0, 600.0)
+    out.append(("c2_trace", t, m))
+    t, m = gen.trace(3, [4.0] * 32, 2.0, 120.0)
+    out.append(("c3_trace_120s", t, m))
+    t, m = gen.trace(5000 + 273, [4.0 * 0.25 * 16.0 ** (1 / 15)] * 32, 8.0 ** (1 / 15), 600.0)
+    out.append(("c5_point273", t, m))
+    return out
+
+
+def test_golden_hashes():
+    with open(GOLDEN) as f:
+        want = json.load(f)
+    for name, t, m in golden_traces():
+        assert _sha(t, m) == want[name]["sha256"], name
+        assert len(t) == want[name]["n"], name
+
+
+def test_deterministic_and_keyed():
+    a = gen.trace(7, [3.0, 1.0], 2.0, 100.0)
+    b = gen.trace(7, [3.0, 1.0], 2.0, 100.0)
+    c = gen.trace(8, [3.0, 1.0], 2.0, 100.0)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    assert not np.array_equal(a[0][:50], c[0][:50])
+
+
+def test_merge_order_and_per_model_streams():
+    rates = [2.0, 0.5, 4.0, 1.0]
+    t, m = gen.trace(11, rates, 4.0, 400.0)
+    assert np.all(np.diff(t) >= 0)
+    # equal timestamps are ordered by model id
+    same = np.diff(t) == 0
+    assert same.any()  # CV 4 produces ties in fp64
+    assert np.all(np.diff(m)[same] >= 0)
+    assert t[0] > 0 and t[-1] < 400.0
+    # each model's subsequence is exactly that model's own stream
+    for mm in range(4):
+        solo = [0.0] * 4
+        solo[mm] = rates[mm]
+        ts, ms = gen.trace(11, solo, 4.0, 400.0)
+        assert np.array_equal(ts, t[m == mm])
+
+
+def test_zero_rate_and_empty():
+    t, m = gen.trace(1, [0.0, 0.0], 1.0, 10.0)
+    assert len(t) == 0
+    t, m = gen.trace(1, [1.0], 1.0, 0.0)
+    assert len(t) == 0
+
+
+@pytest.mark.parametrize("shape", [1.0 / 64, 1.0 / 16, 0.25, 1.0, 4.0])
+def test_gamma_variates_ks(shape):
+    x = gen.gammas(gen.key(99, 7, int(shape * 1000)), shape, 20000)
+    assert np.all(x >= 0)
+    d, p = stats.kstest(x, stats.gamma(shape).cdf)
+    assert p > 1e-3, (shape, d, p)
+
+
+@pytest.mark.parametrize("cv", [1.0, 2.0, 3.0, 4.0])
+def test_gap_mean_and_cv(cv):
+    lam = 2.0
+    n_target = 400000
+    t, _ = gen.trace(123, [lam], cv, n_target / lam)
+    gaps = np.diff(np.concatenate([[0.0], t]))
+    mean = gaps.mean()
+    # standard error of the mean gap is cv/(lam sqrt n); CV estimate is noisier
+    # for heavy tails, so it gets a looser bound
+    assert abs(mean - 1 / lam) < 5 * cv / lam / math.sqrt(len(gaps))
+    est_cv = gaps.std() / mean
+    assert abs(est_cv - cv) < 0.05 * cv + 0.02
+
+
+def test_poisson_counts():
+    lam, T = 5.0, 60.0
+    counts = np.array([len(gen.trace(1000 + s, [lam], 1.0, T)[0]) for s in range(400)])
+    # N(T) ~ Poisson(lam T): mean and variance both lam T
+    assert abs(counts.mean() - lam * T) < 5 * math.sqrt(lam * T / len(counts))
+    assert abs(counts.var() / (lam * T) - 1.0) < 0.25
+
+
+def test_uniforms_and_permutations():
+    u = gen.uniforms(gen.key(1, 2, 3), 100000)
+    assert u.min() > 0 and u.max() < 1
+    assert stats.kstest(u, "uniform").pvalue > 1e-3
+    p = gen.permutations(4, gen.PURPOSE_PERMUTE, 0, 2000, 16)
+    assert np.all(np.sort(p, axis=1) == np.arange(16))
+    # first element close to uniform over the 16 groups
+    counts = np.bincount(p[:, 0], minlength=16)
+    assert stats.chisquare(counts).pvalue > 1e-3
+
+
+def test_problem_shapes():
+    pb = problems.c1_tiny()
+    assert pb.group_cfg.shape == (273, 4) and pb.host_mask.shape == (273, 4)
+    assert 1000 < len(pb.t) < 1400
+    # stage latency of the 4-stage configuration: d (1 + 0.15) / 4
+    assert pb.stage_lat[0, 2, 0] == (0.10 * (1.0 + 0.05 * 3)) * 1.0 / 4
+    pb2 = problems.c2_greedy_step()
+    assert pb2.n_jobs == 512
+    assert np.all((pb2.weight_mib >= 2048) & (pb2.weight_mib < 6144))
+    assert np.all((pb2.d_single >= 0.1) & (pb2.d_single < 0.4))
