@@ -1,0 +1,174 @@
+"""Benchmark of the batched serving simulator on one MI355X.
+
+Workload: the heavy-trace configuration -- 64 models with power-law (0.9)
+rates summing to 1000 req/s, Gamma CV 4, one hour (about 3.6 M requests),
+8192 candidate placements of 16 groups x (S=4, k=2), SLO scale 5, per-request
+outputs kept for 16 of the placements.  One step = one batched call that
+simulates every placement over the whole trace (dispatch, stage recurrence,
+admission, counting, digests, per-request outputs); inputs are resident in HBM
+before the timed region.
+
+Prints ONE JSON line: events/s (request x placement pairs per second), the
+roofline of the simulator kernel, and the CPU oracle's rate on a bounded
+sample of the same workload (single thread), with sampled bit-exact parity.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "simulated request×placement events/sec on 1 GPU; % of HBM/VALU roofline"
+# fp64 vector lane-operations per second on MI355X: 256 CUs x 4 SIMDs x 16
+# fp64 lanes x 2.4 GHz = 3.93e13 (the 78.6 TFLOP/s figure counts an FMA as 2;
+# the simulator issues no FMA, only max / add / compare / multiply).
+PEAK_FP64_OPS = 256 * 4 * 16 * 2.4e9
+HBM_PEAK = 8.0e12
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_ops(pb):
+    """fp64 operations the definition needs per launch: per request of a hosted
+    model, (H - 1) dispatch compares over its H hosting groups, S max + S add in
+    the stage chain, one add for the deadline and one compare; plus one
+    multiply per (job, model) for the SLO.  Placements here give every group
+    the same configuration."""
+    import numpy as np
+    M = pb.d_single.shape[0]
+    counts = np.bincount(pb.model, minlength=M).astype(np.float64)
+    S = int(pb.cfg_stages[pb.group_cfg[0, 0]])
+    hosts = np.zeros(pb.host_mask.shape, dtype=np.float64)
+    hm = pb.host_mask
+    for g in range(64):
+        hosts += ((hm >> np.uint64(g)) & np.uint64(1)).astype(np.float64)
+    per = np.where(hosts > 0, hosts - 1 + 2 * S + 2, 0.0)  # [P, M]
+    ops_per_scale = float((per * counts[None, :]).sum()) + pb.group_cfg.shape[0] * M
+    return ops_per_scale * pb.slo_scale.shape[0]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--placements", type=int, default=8192)
+    ap.add_argument("--duration", type=float, default=3600.0)
+    ap.add_argument("--cpu-sample", type=int, default=64, help="jobs timed on the CPU oracle")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibrate-copy", type=float, default=0.0,
+                    help="instead of the benchmark, run a plain device copy of this many GiB "
+                         "(HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    if args.calibrate_copy > 0:
+        n = int(args.calibrate_copy * (1 << 30)) // 8
+        x = torch.empty(n, dtype=torch.float64, device="cuda")
+        y = torch.empty_like(x)
+        x.fill_(1.0)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_read": n * 8, "bytes_written": n * 8}))
+        return
+
+    from paper_2302_11665_amd import api, sim
+    from paper_2302_11665_amd.workload import problems
+
+    t0 = time.time()
+    pb = problems.c4_heavy(duration=args.duration, n_placements=args.placements)
+    gen_s = time.time() - t0
+    N, J = len(pb.t), pb.n_jobs
+    events = N * J
+    log(f"workload: {J} jobs x {N} requests = {events:.3e} events; trace+placements built in {gen_s:.2f}s")
+    t0 = time.time()
+    dp = api.upload(pb)
+    torch.cuda.synchronize()
+    up_s = time.time() - t0
+    log(f"uploaded in {up_s:.2f}s; library {sim.as_version()}")
+
+    for w in range(args.warmup):
+        api.run(dp)
+        torch.cuda.synchronize()
+        log(f"warmup {w + 1}/{args.warmup} done")
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev[0].record(stream)
+    for k in range(args.steps):
+        api.run(dp)
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    per = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
+    ms = float(np.mean(per))
+    log(f"timed {args.steps} steps: {ms:.2f} ms/step (min {min(per):.2f}, max {max(per):.2f}); wall {wall:.2f}s")
+    value = events / (ms / 1000.0)
+    res = api.results(dp)
+
+    ops = algorithmic_ops(pb)
+    achieved = ops / (ms / 1000.0) / 1e12
+    peak = PEAK_FP64_OPS / 1e12
+    roof = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(peak, 2), "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 5), "traffic": None,
+            "ops_per_event": round(ops / events, 3),
+            "note": "fp64 lane-ops (max/add/cmp/mul, no FMA) of the definition per launch / mean launch time"}
+
+    out = {"metric": METRIC, "value": round(value, 1), "unit": "events/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+           "data": "synthetic",
+           "config": {"workload": "heavy trace: 64 models power-law(0.9) 1000 req/s Gamma CV4 1h; "
+                                  "8192 placements of 16 groups (S=4,k=2); SLO scale 5",
+                      "requests": N, "placements": pb.group_cfg.shape[0], "jobs": J,
+                      "finish_jobs": int(len(pb.finish_jobs))},
+           "roofline": roof, "trace_gen_s": round(gen_s, 3), "upload_s": round(up_s, 3)}
+
+    if not args.no_cpu and args.cpu_sample > 0:
+        import oracle
+        if not os.path.exists(oracle.LIB_PATH):
+            oracle.build()
+        lib = oracle.lib()
+        step = max(1, J // args.cpu_sample)
+        sample = list(range(0, J, step))[: args.cpu_sample]
+        fset = set(int(x) for x in pb.finish_jobs[:2])
+        mism = 0
+        t0 = time.perf_counter()
+        for q, j in enumerate(sample):
+            s, dg, fin = lib.simulate_job(pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat,
+                                          pb.group_cfg[j], pb.host_mask[j], pb.slo_scale[0],
+                                          want_finish=j in fset)
+            if int(res["served"][j]) != s or tuple(int(x) for x in res["digest"][j]) != dg:
+                mism += 1
+            if fin is not None and res["finish"][j].tobytes() != fin.tobytes():
+                mism += 1
+            if q % 16 == 15:
+                log(f"cpu oracle {q + 1}/{len(sample)} jobs")
+        cpu_s = time.perf_counter() - t0
+        # the parity comparisons above are outside the oracle's own work but
+        # negligible next to it
+        cpu_rate = len(sample) * N / cpu_s
+        out["cpu_baseline"] = {"value": round(cpu_rate, 1), "unit": "events/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{len(sample)} of {J} jobs (every {step}th) x full trace = "
+                                         f"{len(sample) * N:.3e} events, single thread, {cpu_s:.1f}s"}
+        out["parity_sampled"] = {"jobs": len(sample), "finish_rows": len(fset), "mismatches": mism}
+        out["speedup_vs_cpu_oracle"] = round(value / cpu_rate, 1)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

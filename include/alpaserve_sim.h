@@ -1,0 +1,161 @@
+/*
+ * alpaserve_sim.h -- C-ABI of libalpaserve_sim.so, the batched serving
+ * simulator for AlpaServe-style placement search on AMD MI355X (gfx950).
+ *
+ * What is computed (AlpaServe, Sec. 4.3, Sec. 3.2, Sec. 3.4, Sec. 4.2):
+ * one "job" is a (trace, placement, SLO scale) triple.  A placement splits the
+ * devices into groups; group g has one parallel configuration c_g with S pipeline
+ * stages and hosts a subset of the models (a model may be hosted by several
+ * groups).  Requests are processed in trace order.  A request for model m at
+ * time t goes to the hosting group with the smallest stage-0 free time (ties to
+ * the lowest group index); its projected finish is
+ *     f_{-1} = t,  f_s = max(f_{s-1}, F[g][s]) + L[m][c_g][s]   (s = 0..S-1)
+ * where F[g][s] is the finish time at stage s of the last request the group
+ * accepted (0 initially).  It is served iff f_{S-1} <= t + scale * d_single[m]
+ * (the product rounded once); then F[g][s] := f_s.  Otherwise it is rejected
+ * and nothing changes (no retry on another group).  A request for a model no
+ * group hosts is a miss.  All arithmetic is IEEE binary64, round to nearest,
+ * no fused multiply-add, in exactly this order, so results are reproducible
+ * bit for bit on any conforming implementation.
+ *
+ * Outputs per job: served = number of served requests; attain = served / n
+ * (0 when n = 0); digest[2] = {h, fin_sum}: accept bits packed 64 per word (bit
+ * i mod 64 of word i div 64, the last word possibly partial), each word w folded
+ * as h = (h XOR w) * 0x9E3779B97F4A7C15 mod 2^64 starting from h = 0, and
+ * fin_sum = sum mod 2^64 of the IEEE-754 bit patterns of served finish times.
+ * Optional per-request output for selected jobs: the finish time of a served
+ * request, -1.0 for a rejected one, -2.0 for a miss.
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers are DEVICE pointers unless marked HOST.  The caller owns every
+ *     buffer; outputs are caller-allocated and fully written.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream); outputs are valid after the stream synchronises.
+ *   - Return 0 (AS_OK) or a negative AS_E_* code; as_last_error() then holds a
+ *     message.  Nothing aborts and no C++ exception crosses this boundary.
+ *   - Scalar arguments and HOST arrays are always checked.  Device data are not
+ *     read by the checks; call as_validate() (synchronous) to check them.
+ *     Invalid device data give unspecified results but never an access outside
+ *     the buffers described here.
+ */
+#ifndef ALPASERVE_SIM_H
+#define ALPASERVE_SIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AS_OK 0
+#define AS_E_INVALID_ARG (-1) /* null pointer, negative size, bad host array    */
+#define AS_E_LIMITS (-2)      /* a size beyond the limits below                  */
+#define AS_E_HIP (-3)         /* a HIP runtime call or kernel launch failed      */
+#define AS_E_NOMEM (-4)       /* device allocation failed                        */
+#define AS_E_INVALID_DATA (-5) /* as_validate found a device-data precondition broken */
+
+#define AS_MAX_MODELS 64   /* M: per-group hosted-model bitmaps are 64 bits wide */
+#define AS_MAX_GROUPS 64   /* G: host_mask rows are 64-bit group bitmaps         */
+#define AS_MAX_STAGES 8    /* S per configuration                                */
+#define AS_MAX_CONFIGS 32  /* C                                                  */
+#define AS_MAX_FINISH 256  /* jobs with per-request output per call              */
+
+/* One arrival trace. */
+typedef struct {
+  int64_t n;            /* number of requests, >= 0                                 */
+  const double* t;      /* [n] arrival times in seconds: finite, >= 0, nondecreasing */
+  const int32_t* model; /* [n] model ids in [0, n_models)                          */
+} as_trace_t;
+
+/* Models and parallel configurations (Sec. 4.1 produces per-configuration
+ * stage latencies; here they are inputs). */
+typedef struct {
+  int32_t n_models;          /* M, 1..AS_MAX_MODELS                               */
+  int32_t n_configs;         /* C, 1..AS_MAX_CONFIGS                              */
+  int32_t max_stages;        /* row length of stage_lat, >= every cfg_stages[c]   */
+  const double* d_single;    /* [M] single-device latency, the SLO base: finite, > 0 */
+  const int32_t* cfg_stages; /* HOST [C] pipeline depth S_c, 1..AS_MAX_STAGES     */
+  const double* stage_lat;   /* [M][C][max_stages] stage latencies in seconds:
+                                finite, >= 0; entries s >= S_c are ignored        */
+} as_models_t;
+
+/* Candidate placements (Sec. 4.2: group partition + model selection + config). */
+typedef struct {
+  int32_t n_placements;      /* P, >= 0                                           */
+  int32_t max_groups;        /* G, 1..AS_MAX_GROUPS                               */
+  const int32_t* group_cfg;  /* [P][G] configuration of group g, -1 = no group    */
+  const uint64_t* host_mask; /* [P][M] bit g set <=> group g hosts model m; only
+                                groups with group_cfg >= 0 may be set            */
+} as_placements_t;
+
+/*
+ * Score every placement at every SLO scale over one shared trace
+ * (Alg. 1's simulate(sel, W) call, batched; Sec. 4.2).
+ *   slo_scale[K]     SLO multiples of d_single: >= 0 (+inf allowed, NaN not)
+ *   jobs             J = P * K, job j = p * K + k (row-major [P][K])
+ *   out_served[J]    served counts
+ *   out_attain[J]    served / n, or NULL
+ *   out_digest[J][2] {h, fin_sum}, or NULL
+ *   finish_jobs      HOST [n_finish] distinct job ids in [0, J), or NULL
+ *   out_finish       [n_finish][trace->n] per-request outputs of those jobs
+ * Each job's state lives in one wavefront: lanes hold the groups of a job
+ * (several jobs per wavefront when the group count allows), arrivals are
+ * staged through LDS in chunks shared by the workgroup.
+ */
+int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
+                           const as_placements_t* placements, const double* slo_scale,
+                           int32_t n_scales, int64_t* out_served, double* out_attain,
+                           uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
+                           double* out_finish, void* stream);
+
+/* A job of the segmented variant. */
+typedef struct {
+  int32_t placement; /* index into the placements                       */
+  int32_t segment;   /* trace segment, index into seg_offsets           */
+  double slo_scale;  /* SLO multiple: >= 0, +inf allowed                */
+} as_job_t;
+
+/*
+ * Jobs that each bring their own trace segment (SLO-curve sweeps: one
+ * placement over many generated workloads).  Segment s is requests
+ * [seg_offsets[s], seg_offsets[s+1]) of t/model, each segment nondecreasing in
+ * t on its own.
+ *   t, model         concatenated segments (device)
+ *   seg_offsets      [n_segments + 1], nondecreasing, seg_offsets[0] = 0 (device)
+ *   jobs             [n_jobs] (device)
+ *   out_*            as above, indexed by job; attain = served / segment length
+ *   out_finish       [n_finish][finish_stride]; row f receives job
+ *                    finish_jobs[f]'s outputs for requests i < min(segment
+ *                    length, finish_stride)
+ */
+int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,
+                     int32_t n_segments, const as_models_t* models,
+                     const as_placements_t* placements, const as_job_t* jobs, int32_t n_jobs,
+                     int64_t* out_served, double* out_attain, uint64_t* out_digest,
+                     const int32_t* finish_jobs, int32_t n_finish, double* out_finish,
+                     int64_t finish_stride, void* stream);
+
+/*
+ * Check the device-data preconditions of as_simulate_placements (trace
+ * sorted, finite and >= 0; model ids in range; group configurations in
+ * [-1, C); host_mask bits only on existing groups; latencies finite and >= 0;
+ * d_single finite and > 0; scales >= 0 and not NaN).  Synchronous: returns
+ * AS_OK, AS_E_INVALID_DATA with a message naming the first failed check, or
+ * another AS_E_* code.  Allocates a few bytes of device memory per call.
+ */
+int as_validate(const as_trace_t* trace, const as_models_t* models,
+                const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
+                void* stream);
+
+/* Message of the last failed call on this thread ("" if none); valid until
+ * the next call on this thread. */
+const char* as_last_error(void);
+
+/* Library version string. */
+const char* as_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALPASERVE_SIM_H */

@@ -1,0 +1,340 @@
+// C-ABI of the batched serving simulator: argument checks, kernel selection,
+// launches on the caller's stream, error reporting.  See alpaserve_sim.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "alpaserve_sim.h"
+#include "sim_kernel.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return AS_OK;
+}
+
+int pow2ceil(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+using as_dev::KArgs;
+
+// LDS bytes of one workgroup for lanes-per-job W and padded stage count SMAX.
+size_t lds_bytes(int W, int SMAX, bool seg, int M, int C) {
+  const int slots = (64 / W) * as_dev::kWaves;
+  int ch = as_dev::kChunk;
+  if (seg) {
+    ch = 4096 / slots;
+    if (ch > 128) ch = 128;
+    if (ch < 16) ch = 16;
+    ch *= slots;
+  }
+  return (size_t)M * C * SMAX * 8 + (size_t)slots * M * 8 + (size_t)ch * 12;
+}
+
+constexpr size_t kMaxLds = 64 * 1024;
+
+template <int W, int SMAX, bool SEG>
+hipError_t launch_t(const KArgs& a, size_t lds, hipStream_t s) {
+  constexpr int slots = (64 / W) * as_dev::kWaves;
+  const int grid = (a.J + slots - 1) / slots;
+  hipLaunchKernelGGL((as_dev::sim_kernel<W, SMAX, SEG>), dim3(grid), dim3(as_dev::kThreads), lds, s,
+                     a);
+  return hipGetLastError();
+}
+
+template <int W, bool SEG>
+hipError_t launch_s(int smax, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (smax) {
+    case 1: return launch_t<W, 1, SEG>(a, lds, s);
+    case 2: return launch_t<W, 2, SEG>(a, lds, s);
+    case 4: return launch_t<W, 4, SEG>(a, lds, s);
+    default: return launch_t<W, 8, SEG>(a, lds, s);
+  }
+}
+
+template <bool SEG>
+hipError_t launch(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (W) {
+    case 1: return launch_s<1, SEG>(smax, a, lds, s);
+    case 2: return launch_s<2, SEG>(smax, a, lds, s);
+    case 4: return launch_s<4, SEG>(smax, a, lds, s);
+    case 8: return launch_s<8, SEG>(smax, a, lds, s);
+    case 16: return launch_s<16, SEG>(smax, a, lds, s);
+    case 32: return launch_s<32, SEG>(smax, a, lds, s);
+    default: return launch_s<64, SEG>(smax, a, lds, s);
+  }
+}
+
+// Checks shared by both simulate entry points; fills the model/placement part
+// of KArgs and the kernel shape.
+int check_common(const as_models_t* models, const as_placements_t* plc, KArgs& a, int& W,
+                 int& smax) {
+  if (!models || !plc) return fail(AS_E_INVALID_ARG, "models and placements must not be NULL");
+  const as_models_t& md = *models;
+  const as_placements_t& pl = *plc;
+  if (md.n_models < 1 || md.n_models > AS_MAX_MODELS)
+    return fail(md.n_models < 1 ? AS_E_INVALID_ARG : AS_E_LIMITS, "n_models=%d outside 1..%d",
+                md.n_models, AS_MAX_MODELS);
+  if (md.n_configs < 1 || md.n_configs > AS_MAX_CONFIGS)
+    return fail(md.n_configs < 1 ? AS_E_INVALID_ARG : AS_E_LIMITS, "n_configs=%d outside 1..%d",
+                md.n_configs, AS_MAX_CONFIGS);
+  if (md.max_stages < 1) return fail(AS_E_INVALID_ARG, "max_stages=%d < 1", md.max_stages);
+  if (!md.d_single || !md.stage_lat || !md.cfg_stages)
+    return fail(AS_E_INVALID_ARG, "d_single, cfg_stages and stage_lat must not be NULL");
+  int smax_used = 1;
+  for (int c = 0; c < md.n_configs; ++c) {
+    const int S = md.cfg_stages[c];
+    if (S < 1 || S > md.max_stages)
+      return fail(AS_E_INVALID_ARG, "cfg_stages[%d]=%d outside 1..max_stages=%d", c, S, md.max_stages);
+    if (S > AS_MAX_STAGES)
+      return fail(AS_E_LIMITS, "cfg_stages[%d]=%d > %d", c, S, AS_MAX_STAGES);
+    if (S > smax_used) smax_used = S;
+  }
+  if (pl.n_placements < 0) return fail(AS_E_INVALID_ARG, "n_placements=%d < 0", pl.n_placements);
+  if (pl.max_groups < 1 || pl.max_groups > AS_MAX_GROUPS)
+    return fail(pl.max_groups < 1 ? AS_E_INVALID_ARG : AS_E_LIMITS, "max_groups=%d outside 1..%d",
+                pl.max_groups, AS_MAX_GROUPS);
+  if (pl.n_placements > 0 && (!pl.group_cfg || !pl.host_mask))
+    return fail(AS_E_INVALID_ARG, "group_cfg and host_mask must not be NULL");
+  a.d_single = md.d_single;
+  a.stage_lat = md.stage_lat;
+  a.group_cfg = pl.group_cfg;
+  a.host_mask = pl.host_mask;
+  a.M = md.n_models;
+  a.C = md.n_configs;
+  a.smax_in = md.max_stages;
+  a.G = pl.max_groups;
+  a.P = pl.n_placements;
+  for (int c = 0; c < AS_MAX_CONFIGS; ++c) a.cfg_stages[c] = c < md.n_configs ? md.cfg_stages[c] : 1;
+  W = pow2ceil(pl.max_groups);
+  smax = pow2ceil(smax_used);
+  return AS_OK;
+}
+
+int check_finish(const int32_t* finish_jobs, int32_t n_finish, double* out_finish, int64_t J,
+                 KArgs& a) {
+  if (n_finish < 0) return fail(AS_E_INVALID_ARG, "n_finish=%d < 0", n_finish);
+  if (n_finish > AS_MAX_FINISH) return fail(AS_E_LIMITS, "n_finish=%d > %d", n_finish, AS_MAX_FINISH);
+  if (n_finish > 0 && (!finish_jobs || !out_finish))
+    return fail(AS_E_INVALID_ARG, "finish_jobs and out_finish must not be NULL when n_finish > 0");
+  for (int f = 0; f < n_finish; ++f) {
+    if (finish_jobs[f] < 0 || finish_jobs[f] >= J)
+      return fail(AS_E_INVALID_ARG, "finish_jobs[%d]=%d outside [0, %lld)", f, finish_jobs[f],
+                  (long long)J);
+    for (int q = 0; q < f; ++q)
+      if (finish_jobs[q] == finish_jobs[f])
+        return fail(AS_E_INVALID_ARG, "finish_jobs[%d] repeats job %d", f, finish_jobs[f]);
+    a.finish_jobs[f] = finish_jobs[f];
+  }
+  a.n_finish = n_finish;
+  a.out_finish = out_finish;
+  return AS_OK;
+}
+
+
+// ---------------------------------------------------------------- validation
+enum : uint32_t {
+  V_T_ORDER = 1u << 0,   // t not finite, negative or decreasing
+  V_MODEL = 1u << 1,     // model id out of range
+  V_CFG = 1u << 2,       // group configuration outside [-1, C)
+  V_MASK = 1u << 3,      // hosting bit on a missing group
+  V_LAT = 1u << 4,       // stage latency not finite or negative
+  V_DSINGLE = 1u << 5,   // d_single not finite or not positive
+  V_SCALE = 1u << 6,     // SLO scale negative or NaN
+};
+const char* kValidateMsg[] = {
+    "trace times must be finite, >= 0 and nondecreasing",
+    "model ids must lie in [0, n_models)",
+    "group_cfg entries must lie in [-1, n_configs)",
+    "host_mask may only set bits of groups with group_cfg >= 0",
+    "stage latencies (s < S_c) must be finite and >= 0",
+    "d_single must be finite and > 0",
+    "slo_scale must be >= 0 and not NaN",
+};
+
+__global__ void validate_kernel(const double* t, const int32_t* model, int64_t n, int M, int C,
+                                const int32_t* group_cfg, const uint64_t* host_mask, int64_t P, int G,
+                                const double* stage_lat, int smax_in, const double* d_single,
+                                const double* scales, int K, KArgs cfgs, uint32_t* flags) {
+  uint32_t bad = 0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t tid0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int64_t i = tid0; i < n; i += stride) {
+    const double ti = t[i];
+    if (!(ti >= 0.0) || !(ti <= 1.7976931348623157e308)) bad |= V_T_ORDER;
+    if (i > 0 && !(t[i - 1] <= ti)) bad |= V_T_ORDER;
+    const int32_t m = model[i];
+    if (m < 0 || m >= M) bad |= V_MODEL;
+  }
+  for (int64_t j = tid0; j < P * G; j += stride) {
+    const int32_t c = group_cfg[j];
+    if (c < -1 || c >= C) bad |= V_CFG;
+  }
+  for (int64_t j = tid0; j < P * M; j += stride) {
+    const int64_t p = j / M;
+    const uint64_t mask = host_mask[j];
+    for (int g = 0; g < 64; ++g)
+      if ((mask >> g) & 1u)
+        if (g >= G || group_cfg[p * G + g] < 0) bad |= V_MASK;
+  }
+  for (int64_t j = tid0; j < (int64_t)M * C * smax_in; j += stride) {
+    const int s = (int)(j % smax_in);
+    const int c = (int)((j / smax_in) % C);
+    const double v = stage_lat[j];
+    if (s < cfgs.cfg_stages[c] && (!(v >= 0.0) || !(v <= 1.7976931348623157e308))) bad |= V_LAT;
+  }
+  for (int64_t j = tid0; j < M; j += stride) {
+    const double d = d_single[j];
+    if (!(d > 0.0) || !(d <= 1.7976931348623157e308)) bad |= V_DSINGLE;
+  }
+  for (int64_t j = tid0; j < K; j += stride)
+    if (!(scales[j] >= 0.0)) bad |= V_SCALE;
+  if (bad) atomicOr(flags, bad);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* as_last_error(void) { return g_err.c_str(); }
+
+const char* as_version(void) { return "alpaserve_sim 0.1 gfx950"; }
+
+int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
+                           const as_placements_t* placements, const double* slo_scale,
+                           int32_t n_scales, int64_t* out_served, double* out_attain,
+                           uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
+                           double* out_finish, void* stream) {
+  KArgs a;
+  std::memset(&a, 0, sizeof a);
+  if (!trace) return fail(AS_E_INVALID_ARG, "trace must not be NULL");
+  if (trace->n < 0) return fail(AS_E_INVALID_ARG, "trace n=%lld < 0", (long long)trace->n);
+  if (trace->n > 0 && (!trace->t || !trace->model))
+    return fail(AS_E_INVALID_ARG, "trace arrays must not be NULL");
+  int W = 1, smax = 1;
+  int rc = check_common(models, placements, a, W, smax);
+  if (rc != AS_OK) return rc;
+  if (n_scales < 0) return fail(AS_E_INVALID_ARG, "n_scales=%d < 0", n_scales);
+  const int64_t J = (int64_t)placements->n_placements * n_scales;
+  if (J > 0x7FFFFFFFLL) return fail(AS_E_LIMITS, "placements x scales = %lld jobs > 2^31-1", (long long)J);
+  if (J > 0 && (!slo_scale || !out_served))
+    return fail(AS_E_INVALID_ARG, "slo_scale and out_served must not be NULL");
+  rc = check_finish(finish_jobs, n_finish, out_finish, J, a);
+  if (rc != AS_OK) return rc;
+  if (J == 0) return ok();
+  a.t = trace->t;
+  a.model = trace->model;
+  a.n = trace->n;
+  a.slo_scale = slo_scale;
+  a.K = n_scales;
+  a.J = (int32_t)J;
+  a.out_served = out_served;
+  a.out_attain = out_attain;
+  a.out_digest = out_digest;
+  a.finish_stride = trace->n;
+  const size_t lds = lds_bytes(W, smax, false, a.M, a.C);
+  if (lds > kMaxLds)
+    return fail(AS_E_LIMITS, "tables need %zu B of LDS per workgroup (> %zu): reduce models x configs x stages",
+                lds, kMaxLds);
+  hipError_t e = launch<false>(W, smax, a, lds, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,
+                     int32_t n_segments, const as_models_t* models,
+                     const as_placements_t* placements, const as_job_t* jobs, int32_t n_jobs,
+                     int64_t* out_served, double* out_attain, uint64_t* out_digest,
+                     const int32_t* finish_jobs, int32_t n_finish, double* out_finish,
+                     int64_t finish_stride, void* stream) {
+  KArgs a;
+  std::memset(&a, 0, sizeof a);
+  if (n_segments < 0 || n_jobs < 0) return fail(AS_E_INVALID_ARG, "negative n_segments or n_jobs");
+  int W = 1, smax = 1;
+  int rc = check_common(models, placements, a, W, smax);
+  if (rc != AS_OK) return rc;
+  if (n_jobs > 0 && n_segments < 1)
+    return fail(AS_E_INVALID_ARG, "n_segments must be >= 1 when there are jobs");
+  if (n_jobs > 0 && (!t || !model || !seg_offsets || !jobs || !out_served))
+    return fail(AS_E_INVALID_ARG, "t, model, seg_offsets, jobs and out_served must not be NULL");
+  if (finish_stride < 0) return fail(AS_E_INVALID_ARG, "finish_stride < 0");
+  rc = check_finish(finish_jobs, n_finish, out_finish, n_jobs, a);
+  if (rc != AS_OK) return rc;
+  if (n_jobs == 0) return ok();
+  a.t = t;
+  a.model = model;
+  a.seg_off = seg_offsets;
+  a.n_segments = n_segments;
+  a.jobs = jobs;
+  a.J = n_jobs;
+  a.out_served = out_served;
+  a.out_attain = out_attain;
+  a.out_digest = out_digest;
+  a.finish_stride = finish_stride;
+  const size_t lds = lds_bytes(W, smax, true, a.M, a.C);
+  if (lds > kMaxLds)
+    return fail(AS_E_LIMITS, "tables need %zu B of LDS per workgroup (> %zu)", lds, kMaxLds);
+  hipError_t e = launch<true>(W, smax, a, lds, (hipStream_t)stream);
+  if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int as_validate(const as_trace_t* trace, const as_models_t* models,
+                const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
+                void* stream) {
+  KArgs a;
+  std::memset(&a, 0, sizeof a);
+  if (!trace) return fail(AS_E_INVALID_ARG, "trace must not be NULL");
+  if (trace->n < 0) return fail(AS_E_INVALID_ARG, "trace n=%lld < 0", (long long)trace->n);
+  if (trace->n > 0 && (!trace->t || !trace->model))
+    return fail(AS_E_INVALID_ARG, "trace arrays must not be NULL");
+  int W = 1, smax = 1;
+  int rc = check_common(models, placements, a, W, smax);
+  if (rc != AS_OK) return rc;
+  if (n_scales < 0) return fail(AS_E_INVALID_ARG, "n_scales=%d < 0", n_scales);
+  if (n_scales > 0 && !slo_scale) return fail(AS_E_INVALID_ARG, "slo_scale must not be NULL");
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* d_flags = nullptr;
+  hipError_t e = hipMallocAsync((void**)&d_flags, sizeof(uint32_t), s);
+  if (e != hipSuccess) return fail(AS_E_NOMEM, "hipMallocAsync: %s", hipGetErrorString(e));
+  uint32_t flags = 0;
+  e = hipMemsetAsync(d_flags, 0, sizeof(uint32_t), s);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(validate_kernel, dim3(1024), dim3(256), 0, s, trace->t, trace->model,
+                       trace->n, a.M, a.C, a.group_cfg, a.host_mask,
+                       (int64_t)placements->n_placements, a.G, a.stage_lat, a.smax_in, a.d_single,
+                       slo_scale, n_scales, a, d_flags);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(&flags, d_flags, sizeof flags, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  hipError_t ef = hipFreeAsync(d_flags, s);
+  if (e == hipSuccess) e = ef;
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(AS_E_HIP, "as_validate: %s", hipGetErrorString(e));
+  for (int b = 0; b < 7; ++b)
+    if (flags & (1u << b)) return fail(AS_E_INVALID_DATA, "%s", kValidateMsg[b]);
+  return ok();
+}
+
+}  // extern "C"

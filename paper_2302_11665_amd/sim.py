@@ -1,0 +1,202 @@
+"""Thin ctypes binding of libalpaserve_sim.so (see include/alpaserve_sim.h).
+
+Argument marshalling only: device arrays are torch CUDA tensors (PyTorch is
+used for device memory and streams), host arrays are numpy, calls go to the
+C-ABI unchanged and run on torch's current stream.  Every step of the
+simulation runs in the library's HIP kernels; if the library is not built this
+module raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+AS_OK = 0
+AS_E_INVALID_ARG = -1
+AS_E_LIMITS = -2
+AS_E_HIP = -3
+AS_E_NOMEM = -4
+AS_E_INVALID_DATA = -5
+AS_MAX_FINISH = 256
+
+_P = ctypes.c_void_p
+
+
+class as_trace_t(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("t", _P), ("model", _P)]
+
+
+class as_models_t(ctypes.Structure):
+    _fields_ = [("n_models", ctypes.c_int32), ("n_configs", ctypes.c_int32),
+                ("max_stages", ctypes.c_int32), ("d_single", _P), ("cfg_stages", _P),
+                ("stage_lat", _P)]
+
+
+class as_placements_t(ctypes.Structure):
+    _fields_ = [("n_placements", ctypes.c_int32), ("max_groups", ctypes.c_int32),
+                ("group_cfg", _P), ("host_mask", _P)]
+
+
+class as_job_t(ctypes.Structure):
+    _fields_ = [("placement", ctypes.c_int32), ("segment", ctypes.c_int32),
+                ("slo_scale", ctypes.c_double)]
+
+
+AS_JOB_DTYPE = np.dtype([("placement", np.int32), ("segment", np.int32), ("slo_scale", np.float64)])
+assert AS_JOB_DTYPE.itemsize == ctypes.sizeof(as_job_t) == 16
+
+
+class SimError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.SIM_LIB):
+            raise RuntimeError(f"{_build.SIM_LIB} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(_build.SIM_LIB)
+        L.as_simulate_placements.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t),
+                                             ctypes.POINTER(as_placements_t), _P, ctypes.c_int32,
+                                             _P, _P, _P, _P, ctypes.c_int32, _P, _P]
+        L.as_simulate_placements.restype = ctypes.c_int
+        L.as_simulate_jobs.argtypes = [_P, _P, _P, ctypes.c_int32, ctypes.POINTER(as_models_t),
+                                       ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, _P, _P, _P,
+                                       _P, ctypes.c_int32, _P, ctypes.c_int64, _P]
+        L.as_simulate_jobs.restype = ctypes.c_int
+        L.as_validate.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t),
+                                  ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, _P]
+        L.as_validate.restype = ctypes.c_int
+        L.as_last_error.argtypes = []
+        L.as_last_error.restype = ctypes.c_char_p
+        L.as_version.argtypes = []
+        L.as_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def as_last_error() -> str:
+    return lib().as_last_error().decode()
+
+
+def as_version() -> str:
+    return lib().as_version().decode()
+
+
+def _ptr(x):
+    """Device pointer of a torch tensor, host pointer of a numpy array, or NULL."""
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+def _check(rc):
+    if rc != AS_OK:
+        raise SimError(rc, as_last_error())
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def make_models(d_single, cfg_stages: np.ndarray, stage_lat):
+    """as_models_t over device tensors d_single[M], stage_lat[M, C, Smax] and the
+    host array cfg_stages[C] (kept alive by the returned tuple)."""
+    cfg = np.ascontiguousarray(cfg_stages, dtype=np.int32)
+    M, C, S = stage_lat.shape
+    m = as_models_t(M, C, S, _ptr(d_single), cfg.ctypes.data, _ptr(stage_lat))
+    return m, cfg
+
+
+def make_placements(group_cfg, host_mask):
+    P, G = group_cfg.shape
+    return as_placements_t(P, G, _ptr(group_cfg), _ptr(host_mask))
+
+
+def as_simulate_placements(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
+                           slo_scale, out_served, out_attain=None, out_digest=None,
+                           finish_jobs=None, out_finish=None, stream=None):
+    """Marshal to as_simulate_placements.  Device tensors: t[N] f64, model[N] i32,
+    d_single[M] f64, stage_lat[M,C,Smax] f64, group_cfg[P,G] i32, host_mask[P,M]
+    (int64 storage of the uint64 bitmaps), slo_scale[K] f64, out_served[P*K] i64,
+    out_attain[P*K] f64, out_digest[P*K,2] (int64 storage), out_finish[F,N] f64.
+    Host: cfg_stages[C] i32, finish_jobs[F] i32."""
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    pl = make_placements(group_cfg, host_mask)
+    fj = None if finish_jobs is None else np.ascontiguousarray(finish_jobs, dtype=np.int32)
+    nf = 0 if fj is None else int(fj.shape[0])
+    rc = lib().as_simulate_placements(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl),
+                                      _ptr(slo_scale), int(slo_scale.shape[0]), _ptr(out_served),
+                                      _ptr(out_attain), _ptr(out_digest), _ptr(fj), nf,
+                                      _ptr(out_finish), _stream(stream))
+    _check(rc)
+
+
+def as_simulate_jobs(t, model, seg_offsets, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
+                     jobs, out_served, out_attain=None, out_digest=None, finish_jobs=None,
+                     out_finish=None, finish_stride=0, stream=None):
+    """Marshal to as_simulate_jobs.  jobs: device tensor of as_job_t records
+    (uint8 storage, 16 bytes each) -- see jobs_to_bytes()."""
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    pl = make_placements(group_cfg, host_mask)
+    fj = None if finish_jobs is None else np.ascontiguousarray(finish_jobs, dtype=np.int32)
+    nf = 0 if fj is None else int(fj.shape[0])
+    n_jobs = int(jobs.numel() // AS_JOB_DTYPE.itemsize)
+    rc = lib().as_simulate_jobs(_ptr(t), _ptr(model), _ptr(seg_offsets), int(seg_offsets.shape[0] - 1),
+                                ctypes.byref(md), ctypes.byref(pl), _ptr(jobs), n_jobs,
+                                _ptr(out_served), _ptr(out_attain), _ptr(out_digest), _ptr(fj), nf,
+                                _ptr(out_finish), int(finish_stride), _stream(stream))
+    _check(rc)
+
+
+def as_validate(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
+                stream=None):
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    pl = make_placements(group_cfg, host_mask)
+    rc = lib().as_validate(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl), _ptr(slo_scale),
+                           int(slo_scale.shape[0]), _stream(stream))
+    _check(rc)
+
+
+def jobs_to_bytes(placement, segment, slo_scale) -> np.ndarray:
+    """Pack job records into the as_job_t byte layout (host uint8 array)."""
+    n = len(placement)
+    rec = np.zeros(n, dtype=AS_JOB_DTYPE)
+    rec["placement"] = placement
+    rec["segment"] = segment
+    rec["slo_scale"] = slo_scale
+    return rec.view(np.uint8)
+
+
+# ------------------------------------------------------------------ helpers
+
+def to_device(a, device="cuda"):
+    """numpy -> torch device tensor (uint64 bitmaps travel as int64 storage)."""
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    return torch.from_numpy(a).to(device)
+
+
+def u64(x) -> np.ndarray:
+    """int64 storage (torch tensor or numpy) back to uint64 numpy."""
+    if not isinstance(x, np.ndarray):
+        x = x.cpu().numpy()
+    return x.view(np.uint64)

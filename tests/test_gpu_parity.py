@@ -1,0 +1,199 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle on the
+same seeded inputs, bit-exact.  Sizes are chosen so the oracle finishes in
+seconds while the GPU runs still span several LDS chunks, ragged tails, every
+lanes-per-job shape and every padded stage count."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+from gpu_common import compare, oracle_problem, say  # noqa: E402
+from oracle_pins import random_case  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2302_11665_amd import api, sim
+    say("library:", sim.as_version())
+    return api
+
+
+def test_c1_all_placements(gpu):
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c1_tiny()
+    say("c1_tiny", pb.n_jobs, len(pb.t))
+    res = gpu.simulate_problem(pb)
+    compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), len(pb.t), "c1")
+
+
+def test_c2_greedy_step(gpu):
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c2_greedy_step()
+    say("c2_greedy_step", pb.n_jobs, len(pb.t))
+    res = gpu.simulate_problem(pb)
+    compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), len(pb.t), "c2")
+
+
+def test_c4_reduced_all_jobs(gpu):
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c4_heavy(duration=45.0, n_placements=600, n_finish=7)
+    say("c4 reduced", pb.n_jobs, len(pb.t))
+    res = gpu.simulate_problem(pb)
+    compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), len(pb.t), "c4 reduced")
+
+
+def test_c3_candidate_steps_every_partition(gpu):
+    """Greedy-step job sets of every partition of the 64-device workload:
+    single-replica candidates from the empty selection, and candidates on top
+    of a random memory-feasible partial selection (2 minutes of trace)."""
+    from paper_2302_11665_amd.workload import problems
+    gp = problems.c3_greedy(duration=120.0)
+    rng = np.random.default_rng(3)
+    M = len(gp.d_single)
+    for pi, part in enumerate(gp.partitions):
+        G = len(part["group_cfg"])
+        cands = [(m, g) for m in range(M) for g in range(G)]
+        pick = rng.choice(len(cands), size=min(96, len(cands)), replace=False)
+        base = np.zeros(M, np.uint64)
+        used = np.zeros(G, np.int64)
+        for _ in range(G * 2):  # random partial selection within memory
+            m, g = int(rng.integers(M)), int(rng.integers(G))
+            if used[g] + gp.weight_mib[m] <= part["group_mem_mib"][g]:
+                base[m] = np.uint64(int(base[m]) | (1 << g))
+                used[g] += gp.weight_mib[m]
+        masks = []
+        for q, k in enumerate(pick):
+            m, g = cands[k]
+            row = (base.copy() if q % 2 else np.zeros(M, np.uint64))
+            row[m] = np.uint64(int(row[m]) | (1 << g))
+            masks.append(row)
+        pb = problems.Problem(f"c3_step_{pi}", gp.t, gp.model, gp.d_single, gp.weight_mib, gp.cfg_stages,
+                              gp.cfg_k, gp.stage_lat, np.tile(part["group_cfg"], (len(masks), 1)),
+                              np.array(masks, np.uint64), np.array([gp.slo_scale]),
+                              np.array([0, len(masks) - 1], np.int32))
+        say("c3 partition", pi, part["label"], pb.n_jobs)
+        res = gpu.simulate_problem(pb)
+        compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), len(pb.t), f"c3 p{pi}")
+
+
+def _random_problem(rng, G, S, n, P, K, M=None, mixed=True):
+    """Random problem with exactly G groups, up to S stages, mixed configs."""
+    from paper_2302_11665_amd.workload.problems import Problem
+    M = M or int(rng.integers(1, 9))
+    C = int(rng.integers(1, 5)) if mixed else 1
+    cfg_stages = rng.integers(1, S + 1, C).astype(np.int32)
+    cfg_stages[0] = S
+    L = rng.uniform(0.01, 0.3, (M, C, S))
+    gaps = rng.exponential(0.02, n)
+    gaps[rng.random(n) < 0.2] = 0.0
+    t = np.cumsum(gaps)
+    model = rng.integers(0, M, n).astype(np.int32)
+    gcfg = rng.integers(0, C, (P, G)).astype(np.int32)
+    gcfg[rng.random((P, G)) < 0.1] = -1
+    gcfg[:, 0] = np.maximum(gcfg[:, 0], 0)
+    masks = np.zeros((P, M), np.uint64)
+    for p in range(P):
+        for m in range(M):
+            if rng.random() < 0.15:
+                continue  # unhosted model
+            k = int(rng.integers(1, min(G, 4) + 1))
+            valid = [g for g in range(G) if gcfg[p, g] >= 0]
+            for g in rng.choice(valid, size=min(k, len(valid)), replace=False):
+                masks[p, m] = np.uint64(int(masks[p, m]) | (1 << int(g)))
+    d = L[:, 0, :].sum(axis=1) * rng.uniform(0.5, 1.5, M)
+    scales = np.array(sorted(rng.choice([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 5.0, np.inf], size=K, replace=False)))
+    J = P * K
+    fin = np.unique(rng.integers(0, J, size=min(3, J))).astype(np.int32)
+    return Problem("random", t, model, d, np.zeros(M, np.int64), cfg_stages, np.ones(C, np.int32), L,
+                   gcfg, masks, scales, fin)
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 4, 5, 8, 11, 16, 17, 32, 33, 64])
+def test_random_shapes_every_width(gpu, G):
+    rng = np.random.default_rng(100 + G)
+    for S in (1, 3, 8):
+        n = int(rng.choice([1, 63, 64, 65, 2047, 2049, 4500]))
+        P = int(rng.integers(1, 40))
+        K = int(rng.integers(1, 4))
+        pb = _random_problem(rng, G, S, n, P, K)
+        say("random", G, S, n, P, K)
+        res = gpu.simulate_problem(pb)
+        compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), n, f"random G={G} S={S} n={n}")
+
+
+def test_tiny_cases_like_the_brute_force_pins(gpu):
+    """The random tiny problems the oracle's brute-force pin uses, one call each."""
+    from paper_2302_11665_amd.workload.problems import Problem
+    rng = np.random.default_rng(2024)
+    for k in range(40):
+        t, model, prob, sigma = random_case(rng, dyadic=(k % 2 == 0))
+        G = len(prob["group_cfg"])
+        pb = Problem("tiny", np.asarray(t, float), model, prob["d_single"], np.zeros(len(prob["d_single"]), np.int64),
+                     prob["cfg_stages"], np.ones(len(prob["cfg_stages"]), np.int32), prob["stage_lat"],
+                     prob["group_cfg"].reshape(1, G), prob["host_mask"].reshape(1, -1), np.array([sigma]),
+                     np.array([0], np.int32))
+        res = gpu.simulate_problem(pb)
+        compare(res, oracle_problem(pb, finish_jobs=[0]), len(t), f"tiny {k}")
+
+
+def test_empty_trace_and_zero_jobs(gpu):
+    from paper_2302_11665_amd.workload.problems import Problem
+    rng = np.random.default_rng(1)
+    pb = _random_problem(rng, 4, 2, 10, 5, 2)
+    pb.t = pb.t[:0]
+    pb.model = pb.model[:0]
+    pb.finish_jobs = np.zeros(0, np.int32)
+    res = gpu.simulate_problem(pb)
+    assert np.all(res["served"] == 0) and np.all(res["attain"] == 0.0)
+    assert np.all(res["digest"] == 0)
+
+
+def test_deterministic_repeat(gpu):
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c2_greedy_step(duration=120.0)
+    dp = gpu.upload(pb)
+    gpu.run(dp)
+    a = gpu.results(dp)
+    gpu.run(dp)
+    b = gpu.results(dp)
+    assert np.array_equal(a["served"], b["served"]) and np.array_equal(a["digest"], b["digest"])
+    for j in a["finish"]:
+        assert a["finish"][j].tobytes() == b["finish"][j].tobytes()
+
+
+def test_validate_catches_bad_data(gpu):
+    import torch
+    from paper_2302_11665_amd import sim
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c1_tiny(duration=5.0)
+    d = sim.to_device
+    args = [d(pb.t), d(pb.model), d(pb.d_single), pb.cfg_stages, d(pb.stage_lat), d(pb.group_cfg),
+            d(pb.host_mask), d(pb.slo_scale)]
+    sim.as_validate(*args)
+    bad_t = pb.t.copy()
+    bad_t[3], bad_t[4] = bad_t[4], bad_t[3] + 1.0
+    cases = {
+        0: d(bad_t),
+        1: d(np.where(np.arange(len(pb.model)) == 2, 7, pb.model).astype(np.int32)),
+        6: d(np.array([-1.0])),
+    }
+    for idx, arr in cases.items():
+        a2 = list(args)
+        a2[idx if idx != 6 else 7] = arr
+        with pytest.raises(sim.SimError) as ei:
+            sim.as_validate(*a2)
+        assert ei.value.code == sim.AS_E_INVALID_DATA
+    hm = pb.host_mask.copy()
+    hm[0, 0] = np.uint64(1 << 5)  # group 5 does not exist
+    a2 = list(args)
+    a2[6] = d(hm)
+    with pytest.raises(sim.SimError):
+        sim.as_validate(*a2)
+    torch.cuda.synchronize()
