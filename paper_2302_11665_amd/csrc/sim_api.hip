@@ -5,11 +5,13 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 
 #include "alpaserve_sim.h"
 #include "sim_kernel.hpp"
+#include "sim_shared.hpp"
 
 namespace {
 
@@ -45,44 +47,151 @@ size_t lds_bytes(int W, int SMAX, bool seg, int M, int C) {
   if (seg) {
     ch = 4096 / slots;
     if (ch > 128) ch = 128;
-    if (ch < 16) ch = 16;
+    if (ch < 32) ch = 32;
     ch *= slots;
   }
-  return (size_t)M * C * SMAX * 8 + (size_t)slots * M * 8 + (size_t)ch * 12;
+  return (size_t)M * pow2ceil(C) * SMAX * 8 + (size_t)M * 8 + (size_t)ch * 12;
 }
 
 constexpr size_t kMaxLds = 64 * 1024;
 
-template <int W, int SMAX, bool SEG>
+template <int W, int GPL, int SMAX, bool SEG>
 hipError_t launch_t(const KArgs& a, size_t lds, hipStream_t s) {
   constexpr int slots = (64 / W) * as_dev::kWaves;
   const int grid = (a.J + slots - 1) / slots;
-  hipLaunchKernelGGL((as_dev::sim_kernel<W, SMAX, SEG>), dim3(grid), dim3(as_dev::kThreads), lds, s,
-                     a);
+  hipLaunchKernelGGL((as_dev::sim_kernel<W, GPL, SMAX, SEG>), dim3(grid), dim3(as_dev::kThreads),
+                     lds, s, a);
   return hipGetLastError();
 }
 
-template <int W, bool SEG>
+template <int W, int GPL, bool SEG>
 hipError_t launch_s(int smax, const KArgs& a, size_t lds, hipStream_t s) {
   switch (smax) {
-    case 1: return launch_t<W, 1, SEG>(a, lds, s);
-    case 2: return launch_t<W, 2, SEG>(a, lds, s);
-    case 4: return launch_t<W, 4, SEG>(a, lds, s);
-    default: return launch_t<W, 8, SEG>(a, lds, s);
+    case 1: return launch_t<W, GPL, 1, SEG>(a, lds, s);
+    case 2: return launch_t<W, GPL, 2, SEG>(a, lds, s);
+    case 4: return launch_t<W, GPL, 4, SEG>(a, lds, s);
+    default: return launch_t<W, GPL, 8, SEG>(a, lds, s);
   }
 }
 
-template <bool SEG>
-hipError_t launch(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
+template <int GPL, bool SEG>
+hipError_t launch_w(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
   switch (W) {
-    case 1: return launch_s<1, SEG>(smax, a, lds, s);
-    case 2: return launch_s<2, SEG>(smax, a, lds, s);
-    case 4: return launch_s<4, SEG>(smax, a, lds, s);
-    case 8: return launch_s<8, SEG>(smax, a, lds, s);
-    case 16: return launch_s<16, SEG>(smax, a, lds, s);
-    case 32: return launch_s<32, SEG>(smax, a, lds, s);
-    default: return launch_s<64, SEG>(smax, a, lds, s);
+    case 1: return launch_s<1, GPL, SEG>(smax, a, lds, s);
+    case 2: return launch_s<2, GPL, SEG>(smax, a, lds, s);
+    case 4: return launch_s<4, GPL, SEG>(smax, a, lds, s);
+    case 8: return launch_s<8, GPL, SEG>(smax, a, lds, s);
+    case 16: return launch_s<16, GPL, SEG>(smax, a, lds, s);
+    case 32:
+      if constexpr (GPL <= 2) return launch_s<32, GPL, SEG>(smax, a, lds, s);
+      break;
+    case 64:
+      if constexpr (GPL == 1) return launch_s<64, GPL, SEG>(smax, a, lds, s);
+      break;
   }
+  return hipErrorInvalidValue;
+}
+
+template <bool SEG>
+hipError_t launch(int W, int GPL, int smax, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (GPL) {
+    case 1: return launch_w<1, SEG>(W, smax, a, lds, s);
+    case 2: return launch_w<2, SEG>(W, smax, a, lds, s);
+    default: return launch_w<4, SEG>(W, smax, a, lds, s);
+  }
+}
+
+// SIMDs of the current device (4 per compute unit), cached per device.
+int simd_count() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+  if (cache[dev] == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return 1024;
+    cache[dev] = prop.multiProcessorCount * 4;
+  }
+  return cache[dev];
+}
+
+// Lanes per job W and groups per lane GPL (W * GPL >= G, powers of two).
+// Cost model: a wavefront issues in order, so the time of a launch is about
+// (wavefronts per SIMD, at least 1) x (instructions per request of one
+// wavefront); a lane that carries more groups needs more instructions per
+// request but fewer wavefronts.  Relative instruction counts per request for
+// GPL = 1, 2, 4 are measured values.  Shapes whose LDS tables do not fit are
+// skipped (a wider W means fewer job slots per workgroup).  ALPASERVE_GPL=1|2|4
+// forces GPL.  Returns false when no shape fits.
+bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, int& GPL) {
+  const int Gp = pow2ceil(G);
+  const double instr[3] = {1.0, 1.45, 2.3};
+  const int n_simd = simd_count();
+  int force = 0;
+  if (const char* e = getenv("ALPASERVE_GPL")) force = atoi(e);
+  double best = 1e300;
+  bool found = false;
+  for (int i = 0; i < 3; ++i) {
+    const int gpl = 1 << i;
+    if (gpl > Gp || (force && force != gpl)) continue;
+    for (int w = Gp / gpl; w <= 64 && w * gpl <= 64; w *= 2) {
+      if (lds_bytes(w, smax, seg, M, C) > kMaxLds) continue;
+      const int64_t waves = (J + (64 / w) - 1) / (64 / w);
+      const double occ = (double)waves / n_simd;
+      const double cost = (occ > 1.0 ? occ : 1.0) * instr[i];
+      if (cost < best) {
+        best = cost;
+        W = w;
+        GPL = gpl;
+        found = true;
+      }
+      break;  // the narrowest W that fits is the cheapest for this GPL
+    }
+  }
+  return found;
+}
+
+// ------------------------------------------------------- shared-trace path
+template <int W, int SMAX>
+hipError_t launch_shared_t(const KArgs& a, bool usig, size_t lds, hipStream_t s) {
+  constexpr int slots = (64 / W) * as_dev::kWaves;
+  const int grid = (a.J + slots - 1) / slots;
+  if (usig)
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, true>), dim3(grid), dim3(as_dev::kThreads), lds,
+                       s, a);
+  else
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, false>), dim3(grid), dim3(as_dev::kThreads), lds,
+                       s, a);
+  return hipGetLastError();
+}
+
+template <int W>
+hipError_t launch_shared_s(int smax, const KArgs& a, bool usig, size_t lds, hipStream_t s) {
+  switch (smax) {
+    case 1: return launch_shared_t<W, 1>(a, usig, lds, s);
+    case 2: return launch_shared_t<W, 2>(a, usig, lds, s);
+    case 4: return launch_shared_t<W, 4>(a, usig, lds, s);
+    default: return launch_shared_t<W, 8>(a, usig, lds, s);
+  }
+}
+
+hipError_t launch_shared(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
+  const bool usig = a.K == 1;
+  switch (W) {
+    case 1: return launch_shared_s<1>(smax, a, usig, lds, s);
+    case 2: return launch_shared_s<2>(smax, a, usig, lds, s);
+    case 4: return launch_shared_s<4>(smax, a, usig, lds, s);
+    case 8: return launch_shared_s<8>(smax, a, usig, lds, s);
+    case 16: return launch_shared_s<16>(smax, a, usig, lds, s);
+    case 32: return launch_shared_s<32>(smax, a, usig, lds, s);
+    default: return launch_shared_s<64>(smax, a, usig, lds, s);
+  }
+}
+
+// Which kernel family runs a shared-trace call: the scalar path by default;
+// ALPASERVE_PATH=lds selects the LDS-staged kernel (used by tests to cover both).
+bool use_shared_path() {
+  const char* e = getenv("ALPASERVE_PATH");
+  return !(e && std::strcmp(e, "lds") == 0);
 }
 
 // Checks shared by both simulate entry points; fills the model/placement part
@@ -126,7 +235,7 @@ int check_common(const as_models_t* models, const as_placements_t* plc, KArgs& a
   a.G = pl.max_groups;
   a.P = pl.n_placements;
   for (int c = 0; c < AS_MAX_CONFIGS; ++c) a.cfg_stages[c] = c < md.n_configs ? md.cfg_stages[c] : 1;
-  W = pow2ceil(pl.max_groups);
+  W = pl.max_groups;  // group count; the shape is chosen per call
   smax = pow2ceil(smax_used);
   return AS_OK;
 }
@@ -252,11 +361,24 @@ int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
   a.out_attain = out_attain;
   a.out_digest = out_digest;
   a.finish_stride = trace->n;
+  if (use_shared_path()) {
+    // one group per lane; the narrowest W whose tables fit in LDS
+    int Ws = pow2ceil(a.G);
+    while (Ws < 64 && lds_bytes(Ws, smax, false, a.M, a.C) > kMaxLds) Ws *= 2;
+    const size_t lds = lds_bytes(Ws, smax, false, a.M, a.C);
+    if (lds > kMaxLds)
+      return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
+                  a.M, a.C, smax);
+    hipError_t e = launch_shared(Ws, smax, a, lds, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return ok();
+  }
+  int GPL = 1;
+  if (!choose_shape(a.G, J, false, a.M, a.C, smax, W, GPL))
+    return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
+                a.M, a.C, smax);
   const size_t lds = lds_bytes(W, smax, false, a.M, a.C);
-  if (lds > kMaxLds)
-    return fail(AS_E_LIMITS, "tables need %zu B of LDS per workgroup (> %zu): reduce models x configs x stages",
-                lds, kMaxLds);
-  hipError_t e = launch<false>(W, smax, a, lds, (hipStream_t)stream);
+  hipError_t e = launch<false>(W, GPL, smax, a, lds, (hipStream_t)stream);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -291,10 +413,12 @@ int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_o
   a.out_attain = out_attain;
   a.out_digest = out_digest;
   a.finish_stride = finish_stride;
+  int GPL = 1;
+  if (!choose_shape(a.G, n_jobs, true, a.M, a.C, smax, W, GPL))
+    return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
+                a.M, a.C, smax);
   const size_t lds = lds_bytes(W, smax, true, a.M, a.C);
-  if (lds > kMaxLds)
-    return fail(AS_E_LIMITS, "tables need %zu B of LDS per workgroup (> %zu)", lds, kMaxLds);
-  hipError_t e = launch<true>(W, smax, a, lds, (hipStream_t)stream);
+  hipError_t e = launch<true>(W, GPL, smax, a, lds, (hipStream_t)stream);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -2,27 +2,33 @@
 //
 // One job = one (trace, placement, SLO scale).  Its state is the free time
 // F[g][s] of every stage s of every group g (Sec. 3.4: each pipeline stage is
-// a single server).  Layout: a job owns W consecutive lanes of a wavefront,
-// lane r of the job holds group r (W = next power of two >= the group count);
-// the stage free times of that group live in the lane's registers.  One
-// wavefront therefore carries 64 / W jobs.
+// a single server).  Layout: a job owns W consecutive lanes of a wavefront and
+// each lane owns GPL consecutive groups (lane r holds groups r*GPL .. r*GPL +
+// GPL - 1); a group's stage free times live in the lane's registers.  One
+// wavefront carries 64 / W jobs; W * GPL >= the group count.  The host picks
+// (W, GPL) so that the jobs fill the GPU's SIMDs with as few instructions per
+// job and request as possible.
 //
 // Per request (t, m) the lanes of a job:
-//   1. dispatch (Sec. 4.3): key = F[g][0] if the lane's group hosts m, else +inf;
-//      a butterfly min over the job's W lanes (DPP inside a 16-lane row, lane
-//      shuffles across rows), then the lowest lane holding the minimum wins
-//      (wavefront ballot restricted to the job's lanes below the caller);
-//   2. project (Sec. 3.4): every lane runs its own group's stage chain
-//      f_s = max(f_{s-1}, F[s]) + L[m][c][s]; only the chosen lane's result is used;
-//   3. admit (Sec. 4.3, Sec. 3.2): the chosen lane accepts iff f_{S-1} <= t + slo_m
-//      and then commits F[s] := f_s;
-//   4. count: served, accept bits and the finish-time bit sum accumulate per
-//      lane and are combined over the job's lanes every 64 requests / at the end.
+//   1. dispatch (Sec. 4.3): key = F[g][0] for every local group that hosts m,
+//      +inf otherwise; the lane keeps its smallest key (lowest local group on
+//      ties), a butterfly min over the job's W lanes (DPP inside 16-lane rows,
+//      lane shuffles across rows) yields the job minimum, and the lowest lane
+//      holding it wins (wavefront ballot restricted to the job's lanes below
+//      the caller) -- so ties go to the lowest group index;
+//   2. project (Sec. 3.4): each lane runs the stage chain
+//      f_s = max(f_{s-1}, F[s]) + L[m][c][s] of each of its local groups;
+//   3. admit (Sec. 4.3, Sec. 3.2): the chosen lane accepts iff the chosen
+//      group's f_{S-1} <= t + (scale * d_single[m]) and then commits F[s] := f_s;
+//   4. count: accept decisions shift into a 32-bit register; every 32
+//      requests they become bits of the job's 64-bit accept word, folded into
+//      the digest every 64 requests (and at the end); served counts are the
+//      population counts of the folded words.
 //
 // Arrivals are staged through LDS in chunks loaded with coalesced reads by the
-// whole workgroup; a shared trace is read once per workgroup per chunk, every
-// wavefront then reads the same LDS words (broadcast).  Segmented traces (one
-// per job) are staged per job slot.
+// whole workgroup; a shared trace is read once per workgroup per chunk and
+// every wavefront then reads the same LDS words (broadcast).  Segmented
+// traces (one per job) are staged per job slot.
 //
 // Exactness: max and min are emitted as v_max_f64 / v_min_f64 (exact; no NaN
 // or -0 ever reaches them), additions are single IEEE v_add_f64, no FMA
@@ -37,28 +43,28 @@
 
 namespace as_dev {
 
-constexpr int kWaves = 4;                 // wavefronts per workgroup
+constexpr int kWaves = 4;  // wavefronts per workgroup
 constexpr int kThreads = 64 * kWaves;
-constexpr int kChunk = 2048;              // shared-trace requests per LDS chunk
-// per-job requests per LDS chunk for segmented traces, sized so that all
-// kSlots job slots of a workgroup fit in about 48 KiB
+constexpr int kChunk = 2048;  // shared-trace requests per LDS chunk (multiple of 64)
+// per-job requests per LDS chunk for segmented traces: all job slots of a
+// workgroup share about 48 KiB; a multiple of 32
 template <int kSlots>
 constexpr int seg_chunk() {
-  return (4096 / kSlots) > 128 ? 128 : ((4096 / kSlots) < 16 ? 16 : 4096 / kSlots);
+  return (4096 / kSlots) > 128 ? 128 : ((4096 / kSlots) < 32 ? 32 : 4096 / kSlots);
 }
 constexpr uint64_t kHashMul = 0x9E3779B97F4A7C15ULL;
 
 struct KArgs {
   const double* t;
   const int32_t* model;
-  int64_t n;                 // shared trace length
-  const int64_t* seg_off;    // segmented: [n_segments + 1]
-  const as_job_t* jobs;      // segmented: [J]
+  int64_t n;               // shared trace length
+  const int64_t* seg_off;  // segmented: [n_segments + 1]
+  const as_job_t* jobs;    // segmented: [J]
   const double* d_single;
   const double* stage_lat;
   const int32_t* group_cfg;
   const uint64_t* host_mask;
-  const double* slo_scale;   // shared: [K]
+  const double* slo_scale;  // shared: [K]
   int64_t* out_served;
   double* out_attain;
   uint64_t* out_digest;
@@ -84,14 +90,14 @@ __device__ __forceinline__ double vmin(double a, double b) {
 
 template <int CTRL>
 __device__ __forceinline__ double dpp_f64(double v) {
-  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, 0xF, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xF, 0xF, false);
+  const int lo = __builtin_amdgcn_mov_dpp(__double2loint(v), CTRL, 0xF, 0xF, true);
+  const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(v), CTRL, 0xF, 0xF, true);
   return __hiloint2double(hi, lo);
 }
 
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
 }
 
 // DPP controls: quad_perm [1,0,3,2] (lane ^ 1), quad_perm [2,3,0,1] (lane ^ 2),
@@ -134,79 +140,155 @@ __device__ __forceinline__ uint64_t seg_sum_u64(uint64_t v) {
   return v;
 }
 
-// Per-lane simulation state of one group of one job.
-template <int SMAX>
+// Per-lane simulation state: GPL groups of one job.
+template <int GPL, int SMAX>
 struct LaneState {
-  double F[SMAX];
-  uint64_t served, fin_sum, word, hash;
+  double F[GPL][SMAX];
+  uint64_t fin_sum;  // this lane's accepted finish-time bit sum
+  uint64_t hash;     // job digest (same in every lane of the job)
+  uint64_t served;   // job served count (same in every lane of the job)
+  uint32_t wlo;      // accept bits of the first half of the current 64-block
 };
 
-// The request loop over one LDS chunk.  FINISH: some job of this wavefront
-// keeps per-request outputs.  Returns nothing; state is updated in place.
-template <int W, int SMAX, bool FINISH>
-__device__ __forceinline__ void run_chunk(LaneState<SMAX>& st, const double* __restrict__ cT,
-                                          const int32_t* __restrict__ cM, int cnt, int64_t base,
-                                          int64_t n_job, uint64_t hostbits, uint64_t below,
-                                          const double* __restrict__ lrow_base, int lstride,
-                                          const double* __restrict__ slo_row, int seg_lane,
-                                          int frow, double* __restrict__ out_finish,
-                                          int64_t finish_stride) {
+// Constant per-lane inputs of the request loop.
+template <int GPL>
+struct LaneConst {
+  uint64_t hostbits[GPL];   // bit m: local group k hosts model m
+  const double* lrow[GPL];  // stage-latency row of local group k for model 0
+  int lshift;               // log2 of the per-model row stride (bytes) of the LDS table
+  const double* dsingle;    // single-device latency of every model (LDS)
+  double sigma;             // this job's SLO scale
+  uint64_t below;           // lanes of this job below this lane
+  int seg_lane;
+  int frow;  // per-request output row of this job, -1 if none
+};
+
+// One request (t, m) at trace position i: dispatch, projection, admission,
+// commit; shifts the accept decision into sr.
+template <int W, int GPL, int SMAX, bool FINISH>
+__device__ __forceinline__ void step(LaneState<GPL, SMAX>& st, const LaneConst<GPL>& lc, double ti,
+                                     int mi, int64_t i, uint32_t& sr,
+                                     double* __restrict__ out_finish, int64_t finish_stride) {
   const double kInf = __builtin_inf();
-  for (int e = 0; e < cnt; ++e) {
-    const double ti = cT[e];
-    const int mi = cM[e];
-    const int64_t i = base + e;
+  {
     // 1. dispatch
-    const bool hosted = (hostbits >> mi) & 1u;
-    const double key = hosted ? st.F[0] : kInf;
-    const double mn = seg_min<W>(key);
-    const bool eq = hosted && key == mn;
-    const uint64_t ball = __ballot(eq);
-    const bool chosen = eq && ((ball & below) == 0);
-    // 2. projection through this lane's stage chain
-    const double* L = lrow_base + mi * lstride;
-    double fs[SMAX];
-    double f = ti;
+    double lmin = kInf;
+    int kb = 0;
 #pragma unroll
-    for (int s = 0; s < SMAX; ++s) {
-      fs[s] = vmax(f, st.F[s]) + L[s];
-      f = fs[s];
-    }
-    // 3. admission
-    const double deadline = ti + slo_row[mi];
-    const bool acc = chosen && !(f > deadline);
-    if (acc) {
-#pragma unroll
-      for (int s = 0; s < SMAX; ++s) st.F[s] = fs[s];
-      st.served += 1;
-      st.fin_sum += (uint64_t)__double_as_longlong(f);
-      st.word |= (uint64_t)1 << (i & 63);
-    }
-    if constexpr (FINISH) {
-      if (frow >= 0 && i < finish_stride) {
-        double* dst = out_finish + (int64_t)frow * finish_stride + i;
-        if (chosen) *dst = acc ? f : -1.0;
-        else if (mn == kInf && seg_lane == 0) *dst = -2.0;
+    for (int k = 0; k < GPL; ++k) {
+      const bool hosted = (lc.hostbits[k] >> mi) & 1u;
+      const double key = hosted ? st.F[k][0] : kInf;
+      if (k == 0) {
+        lmin = key;
+      } else if (key < lmin) {
+        lmin = key;
+        kb = k;
       }
     }
-    // 4. fold the accept word of the job every 64 requests and at its end
-    if ((i & 63) == 63 || i == n_job - 1) {
-      const uint64_t w = seg_or<W>(st.word);
-      st.hash = (st.hash ^ w) * kHashMul;
-      st.word = 0;
+    const double mn = seg_min<W>(lmin);
+    const bool eq = (lmin == mn) && (mn != kInf);
+    const uint64_t ball = __builtin_amdgcn_ballot_w64(eq);
+    const bool chosen = eq && ((ball & lc.below) == 0);
+    // 2. projection through the stage chain of every local group
+    double fs[GPL][SMAX];
+#pragma unroll
+    for (int k = 0; k < GPL; ++k) {
+      const double* L = (const double*)((const char*)lc.lrow[k] + ((unsigned)mi << lc.lshift));
+      double f = ti;
+#pragma unroll
+      for (int s = 0; s < SMAX; ++s) {
+        fs[k][s] = vmax(f, st.F[k][s]) + L[s];
+        f = fs[k][s];
+      }
+    }
+    double f = fs[0][SMAX - 1];
+#pragma unroll
+    for (int k = 1; k < GPL; ++k) f = (kb == k) ? fs[k][SMAX - 1] : f;
+    // 3. admission and commit
+    const double deadline = ti + lc.sigma * lc.dsingle[mi];
+    const bool acc = chosen && !(f > deadline);
+#pragma unroll
+    for (int k = 0; k < GPL; ++k) {
+      const bool ak = acc && (GPL == 1 || kb == k);
+#pragma unroll
+      for (int s = 0; s < SMAX; ++s) st.F[k][s] = ak ? fs[k][s] : st.F[k][s];
+    }
+    st.fin_sum += acc ? (uint64_t)__double_as_longlong(f) : 0ull;
+    sr = (sr << 1) | (acc ? 1u : 0u);
+    if constexpr (FINISH) {
+      if (lc.frow >= 0 && i < finish_stride) {
+        double* dst = out_finish + (int64_t)lc.frow * finish_stride + i;
+        if (chosen) *dst = acc ? f : -1.0;
+        else if (mn == kInf && lc.seg_lane == 0) *dst = -2.0;
+      }
     }
   }
 }
 
-template <int W, int SMAX, bool SEG>
+// Requests [i0, i0 + hc) of one LDS chunk, hc <= 32: one 32-request half of a
+// 64-request accept word.  Returns the accept bits (bit e = request i0 + e
+// accepted by this lane).
+template <int W, int GPL, int SMAX, bool FINISH>
+__device__ __forceinline__ uint32_t run_half(LaneState<GPL, SMAX>& st, const LaneConst<GPL>& lc,
+                                             const double* __restrict__ cT,
+                                             const int32_t* __restrict__ cM, int hc, int64_t i0,
+                                             double* __restrict__ out_finish,
+                                             int64_t finish_stride) {
+  uint32_t sr = 0;
+  if (hc == 32) {
+    // full half: fixed trip count, unrolled so LDS reads use immediate
+    // offsets and can be issued ahead of the dependent arithmetic
+#pragma unroll 4
+    for (int e = 0; e < 32; ++e)
+      step<W, GPL, SMAX, FINISH>(st, lc, cT[e], cM[e], i0 + e, sr, out_finish, finish_stride);
+    return __builtin_bitreverse32(sr);
+  }
+  for (int e = 0; e < hc; ++e)
+    step<W, GPL, SMAX, FINISH>(st, lc, cT[e], cM[e], i0 + e, sr, out_finish, finish_stride);
+  // sr holds request e at bit hc-1-e; return request e at bit e
+  return __builtin_bitreverse32(sr) >> (32 - hc);
+}
+
+// All requests of one LDS chunk [base, base + cnt); base is a multiple of 64
+// and cnt a multiple of 32 unless the job ends inside the chunk.
+template <int W, int GPL, int SMAX, bool FINISH>
+__device__ __forceinline__ void run_chunk(LaneState<GPL, SMAX>& st, const LaneConst<GPL>& lc,
+                                          const double* __restrict__ cT,
+                                          const int32_t* __restrict__ cM, int cnt, int64_t base,
+                                          int64_t n_job, double* __restrict__ out_finish,
+                                          int64_t finish_stride) {
+  for (int h = 0; h < cnt; h += 32) {
+    const int hc = (cnt - h) < 32 ? (cnt - h) : 32;
+    const uint32_t bits = run_half<W, GPL, SMAX, FINISH>(st, lc, cT + h, cM + h, hc, base + h,
+                                                         out_finish, finish_stride);
+    const int64_t pos = (base + h) & 63;  // 0 or 32
+    const bool job_end = base + h + hc == n_job;
+    if (pos == 0 && !job_end) {
+      st.wlo = bits;
+    } else {
+      const uint64_t w = pos == 0 ? (uint64_t)bits : (((uint64_t)bits << 32) | st.wlo);
+      const uint64_t wj = seg_or<W>(w);
+      st.hash = (st.hash ^ wj) * kHashMul;
+      st.served += (uint64_t)__popcll(wj);
+      st.wlo = 0;
+    }
+  }
+}
+
+template <int W, int GPL, int SMAX, bool SEG>
 __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
-  constexpr int JW = 64 / W;                 // jobs per wavefront
-  constexpr int kSlots = JW * kWaves;        // jobs per workgroup
-  extern __shared__ __align__(16) unsigned char smem[];
-  double* sL = reinterpret_cast<double*>(smem);                      // [M][C][SMAX]
-  double* sSlo = sL + (size_t)a.M * a.C * SMAX;                      // [kSlots][M]
-  double* sT = sSlo + (size_t)kSlots * a.M;                          // chunk times
+  constexpr int JW = 64 / W;           // jobs per wavefront
+  constexpr int kSlots = JW * kWaves;  // jobs per workgroup
   constexpr int CH = SEG ? seg_chunk<kSlots>() : kChunk;
+  extern __shared__ __align__(16) unsigned char smem[];
+  // stage-latency table [M][Cp][SMAX], Cp = C rounded up to a power of two so
+  // that a model's rows start at m << lshift bytes
+  int cp = 1, lshift = 0;
+  while (cp < a.C) cp <<= 1;
+  while ((1 << lshift) < cp * SMAX * 8) ++lshift;
+  double* sL = reinterpret_cast<double*>(smem);
+  double* sD = sL + (size_t)a.M * cp * SMAX;     // [M] d_single
+  double* sT = sD + a.M;                         // chunk times
   int32_t* sM = reinterpret_cast<int32_t*>(sT + (SEG ? kSlots * CH : kChunk));
   __shared__ unsigned long long s_nmax;
 
@@ -216,11 +298,11 @@ __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
   const int seg_lane = lane & (W - 1);
   const int slot = wave * JW + lane / W;
   const int64_t job = (int64_t)blockIdx.x * kSlots + slot;
-  bool job_ok = job < a.J;
+  const bool job_ok = job < a.J;
 
   int p = 0;
   double sigma = 0.0;
-  int64_t seg_begin = 0, n_job = a.n;
+  int64_t seg_begin = 0, n_job = SEG ? 0 : a.n;
   if (job_ok) {
     if constexpr (SEG) {
       // job records are device data: a record naming a missing placement or
@@ -231,7 +313,6 @@ __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
       sigma = jb.slo_scale;
       if (p < 0 || p >= a.P || jb.segment < 0 || jb.segment >= a.n_segments) {
         p = 0;
-        n_job = 0;
       } else {
         const int64_t total = a.seg_off[a.n_segments];
         int64_t b = a.seg_off[jb.segment], e = a.seg_off[jb.segment + 1];
@@ -244,44 +325,57 @@ __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
       p = (int)(job / a.K);
       sigma = a.slo_scale[job % a.K];
     }
-  } else {
-    n_job = SEG ? 0 : a.n;
   }
 
-  // this lane's group
-  const int g = seg_lane;
-  int cfg = -1;
-  if (job_ok && g < a.G) cfg = a.group_cfg[(int64_t)p * a.G + g];
-  if (cfg >= a.C) cfg = -1;
-  uint64_t hostbits = 0;
-  if (cfg >= 0) {
-    const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
-    for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> g) & 1u) << m;
+  // this lane's groups
+  LaneConst<GPL> lc;
+#pragma unroll
+  for (int k = 0; k < GPL; ++k) {
+    const int g = seg_lane * GPL + k;
+    int c = -1;
+    if (job_ok && g < a.G) c = a.group_cfg[(int64_t)p * a.G + g];
+    if (c >= a.C || c < 0) c = -1;
+    uint64_t hb = 0;
+    if (c >= 0) {
+      const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
+      for (int m = 0; m < a.M; ++m) hb |= ((hm[m] >> g) & 1u) << m;
+    }
+    lc.hostbits[k] = hb;
+    lc.lrow[k] = sL + (c < 0 ? 0 : c) * SMAX;
   }
-  const int seg_start = lane & ~(W - 1);
-  const uint64_t lt_lane = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const uint64_t lt_start = (seg_start == 0) ? 0ull : (~0ull >> (64 - seg_start));
-  const uint64_t below = lt_lane & ~lt_start;
-
-  // finish-output row of this job (first match)
-  int frow = -1;
+  lc.lshift = lshift;
+  lc.dsingle = sD;
+  lc.sigma = sigma;
+  lc.seg_lane = seg_lane;
+  {
+    const int seg_start = lane & ~(W - 1);
+    const uint64_t lt_lane = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const uint64_t lt_start = (seg_start == 0) ? 0ull : (~0ull >> (64 - seg_start));
+    lc.below = lt_lane & ~lt_start;
+  }
+  // per-request output row of this job (first match)
+  lc.frow = -1;
   if (job_ok)
     for (int f = 0; f < a.n_finish; ++f)
-      if (a.finish_jobs[f] == job) { frow = f; break; }
-  const bool wave_finish = __ballot(frow >= 0) != 0;
+      if (a.finish_jobs[f] == job) {
+        lc.frow = f;
+        break;
+      }
+  const bool wave_finish = __ballot(lc.frow >= 0) != 0;
 
   // stage-latency table, padded with zero-latency stages up to SMAX; a padded
   // stage adds exactly 0 to a finish time that already dominates its free time
-  const int nL = a.M * a.C * SMAX;
+  const int nL = a.M * cp * SMAX;
   for (int idx = tid; idx < nL; idx += kThreads) {
     const int s = idx % SMAX;
     const int mc = idx / SMAX;
-    const int c = mc % a.C;
-    const int m = mc / a.C;
-    sL[idx] = (s < a.cfg_stages[c]) ? a.stage_lat[((int64_t)m * a.C + c) * a.smax_in + s] : 0.0;
+    const int c = mc % cp;
+    const int m = mc / cp;
+    sL[idx] = (c < a.C && s < a.cfg_stages[c])
+                  ? a.stage_lat[((int64_t)m * a.C + c) * a.smax_in + s]
+                  : 0.0;
   }
-  // SLO of every model for this job: scale * d_single[m], one rounding
-  for (int m = seg_lane; m < a.M; m += W) sSlo[slot * a.M + m] = job_ok ? sigma * a.d_single[m] : 0.0;
+  for (int m = tid; m < a.M; m += kThreads) sD[m] = a.d_single[m];
   if (tid == 0) s_nmax = 0;
   __syncthreads();
   if constexpr (SEG) {
@@ -290,15 +384,13 @@ __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
   __syncthreads();
   const int64_t n_loop = SEG ? (int64_t)s_nmax : a.n;
 
-  LaneState<SMAX> st;
+  LaneState<GPL, SMAX> st;
 #pragma unroll
-  for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
-  st.served = st.fin_sum = st.word = st.hash = 0;
-
-  // L row of (m, cfg) is lrow_base + m * lstride
-  const double* lrow_base = sL + (cfg < 0 ? 0 : cfg) * SMAX;
-  const int lstride = a.C * SMAX;
-  const double* slo_row = sSlo + slot * a.M;
+  for (int k = 0; k < GPL; ++k)
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) st.F[k][s] = 0.0;
+  st.fin_sum = st.hash = st.served = 0;
+  st.wlo = 0;
 
   for (int64_t base = 0; base < n_loop; base += CH) {
     const int cnt_all = (int)((n_loop - base) < CH ? (n_loop - base) : CH);
@@ -325,19 +417,16 @@ __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
       cnt = rem <= 0 ? 0 : (rem < CH ? (int)rem : CH);
     }
     if (wave_finish)
-      run_chunk<W, SMAX, true>(st, cT, cM, cnt, base, n_job, hostbits, below, lrow_base, lstride, slo_row,
-                               seg_lane, frow, a.out_finish, a.finish_stride);
+      run_chunk<W, GPL, SMAX, true>(st, lc, cT, cM, cnt, base, n_job, a.out_finish, a.finish_stride);
     else
-      run_chunk<W, SMAX, false>(st, cT, cM, cnt, base, n_job, hostbits, below, lrow_base, lstride, slo_row,
-                                seg_lane, frow, a.out_finish, a.finish_stride);
+      run_chunk<W, GPL, SMAX, false>(st, lc, cT, cM, cnt, base, n_job, a.out_finish, a.finish_stride);
   }
 
   // combine the job's lanes and write its outputs
-  const uint64_t served = seg_sum_u64<W>(st.served);
   const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum);
   if (job_ok && seg_lane == 0) {
-    a.out_served[job] = (int64_t)served;
-    if (a.out_attain) a.out_attain[job] = n_job > 0 ? (double)served / (double)n_job : 0.0;
+    a.out_served[job] = (int64_t)st.served;
+    if (a.out_attain) a.out_attain[job] = n_job > 0 ? (double)st.served / (double)n_job : 0.0;
     if (a.out_digest) {
       a.out_digest[2 * job] = st.hash;
       a.out_digest[2 * job + 1] = fin_sum;
