@@ -18,7 +18,10 @@ INCLUDE = os.path.join(ROOT, "include")
 GEN_SRC = os.path.join(PKG, "workload", "gen.c")
 GEN_LIB = os.path.join(BUILD, "libas_gen.so")
 
-SIM_SRCS = [os.path.join(PKG, "csrc", "sim_api.hip")]
+CSRC = os.path.join(PKG, "csrc")
+SIM_API_SRC = os.path.join(CSRC, "sim_api.hip")
+SIM_LAUNCH_SRC = os.path.join(CSRC, "sim_launch.hip")
+LANE_WIDTHS = (1, 2, 4, 8, 16, 32, 64)  # one launcher translation unit per width
 SIM_LIB = os.path.join(BUILD, "libalpaserve_sim.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -49,10 +52,27 @@ def build_gen() -> str:
     return GEN_LIB
 
 
-def build_sim(extra_flags=()) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build_sim(extra_flags=(), jobs=None) -> str:
+    """Compile the launcher units (one per lane width) and the API unit in
+    parallel, then link the shared library."""
+    from concurrent.futures import ThreadPoolExecutor
+    obj_dir = os.path.join(BUILD, "obj")
+    os.makedirs(obj_dir, exist_ok=True)
+    compile_flags = [f for f in HIP_FLAGS if f != "-shared"]
+    units = [(SIM_API_SRC, os.path.join(obj_dir, "sim_api.o"), [])]
+    for w in LANE_WIDTHS:
+        units.append((SIM_LAUNCH_SRC, os.path.join(obj_dir, f"sim_launch_w{w}.o"), [f"-DAS_W={w}"]))
+
+    def compile_one(u):
+        src, obj, defs = u
+        _run([HIPCC, *compile_flags, *extra_flags, *defs, "-I", INCLUDE, "-I", CSRC, "-c", "-o", obj, src])
+        return obj
+
+    n = jobs or min(len(units), os.cpu_count() or 1)
+    with ThreadPoolExecutor(n) as ex:
+        objs = list(ex.map(compile_one, units))
     tmp = SIM_LIB + ".tmp"
-    _run([HIPCC, *HIP_FLAGS, *extra_flags, "-I", INCLUDE, "-o", tmp, *SIM_SRCS])
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, SIM_LIB)
     return SIM_LIB
 

@@ -11,7 +11,7 @@
 
 #include "alpaserve_sim.h"
 #include "sim_kernel.hpp"
-#include "sim_shared.hpp"
+#include "sim_launch.hpp"
 
 namespace {
 
@@ -55,49 +55,29 @@ size_t lds_bytes(int W, int SMAX, bool seg, int M, int C) {
 
 constexpr size_t kMaxLds = 64 * 1024;
 
-template <int W, int GPL, int SMAX, bool SEG>
-hipError_t launch_t(const KArgs& a, size_t lds, hipStream_t s) {
-  constexpr int slots = (64 / W) * as_dev::kWaves;
-  const int grid = (a.J + slots - 1) / slots;
-  hipLaunchKernelGGL((as_dev::sim_kernel<W, GPL, SMAX, SEG>), dim3(grid), dim3(as_dev::kThreads),
-                     lds, s, a);
-  return hipGetLastError();
-}
 
-template <int W, int GPL, bool SEG>
-hipError_t launch_s(int smax, const KArgs& a, size_t lds, hipStream_t s) {
-  switch (smax) {
-    case 1: return launch_t<W, GPL, 1, SEG>(a, lds, s);
-    case 2: return launch_t<W, GPL, 2, SEG>(a, lds, s);
-    case 4: return launch_t<W, GPL, 4, SEG>(a, lds, s);
-    default: return launch_t<W, GPL, 8, SEG>(a, lds, s);
-  }
-}
-
-template <int GPL, bool SEG>
-hipError_t launch_w(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
+hipError_t launch_lds_any(int W, int gpl, int smax, bool seg, const KArgs& a, size_t lds, hipStream_t s) {
   switch (W) {
-    case 1: return launch_s<1, GPL, SEG>(smax, a, lds, s);
-    case 2: return launch_s<2, GPL, SEG>(smax, a, lds, s);
-    case 4: return launch_s<4, GPL, SEG>(smax, a, lds, s);
-    case 8: return launch_s<8, GPL, SEG>(smax, a, lds, s);
-    case 16: return launch_s<16, GPL, SEG>(smax, a, lds, s);
-    case 32:
-      if constexpr (GPL <= 2) return launch_s<32, GPL, SEG>(smax, a, lds, s);
-      break;
-    case 64:
-      if constexpr (GPL == 1) return launch_s<64, GPL, SEG>(smax, a, lds, s);
-      break;
+    case 1: return as_host::launch_lds<1>(gpl, smax, seg, a, lds, s);
+    case 2: return as_host::launch_lds<2>(gpl, smax, seg, a, lds, s);
+    case 4: return as_host::launch_lds<4>(gpl, smax, seg, a, lds, s);
+    case 8: return as_host::launch_lds<8>(gpl, smax, seg, a, lds, s);
+    case 16: return as_host::launch_lds<16>(gpl, smax, seg, a, lds, s);
+    case 32: return as_host::launch_lds<32>(gpl, smax, seg, a, lds, s);
+    default: return as_host::launch_lds<64>(gpl, smax, seg, a, lds, s);
   }
-  return hipErrorInvalidValue;
 }
 
-template <bool SEG>
-hipError_t launch(int W, int GPL, int smax, const KArgs& a, size_t lds, hipStream_t s) {
-  switch (GPL) {
-    case 1: return launch_w<1, SEG>(W, smax, a, lds, s);
-    case 2: return launch_w<2, SEG>(W, smax, a, lds, s);
-    default: return launch_w<4, SEG>(W, smax, a, lds, s);
+hipError_t launch_shared_any(int W, int jpl, int smax, bool usig, const KArgs& a, size_t lds,
+                             hipStream_t s) {
+  switch (W) {
+    case 1: return as_host::launch_shared<1>(jpl, smax, usig, a, lds, s);
+    case 2: return as_host::launch_shared<2>(jpl, smax, usig, a, lds, s);
+    case 4: return as_host::launch_shared<4>(jpl, smax, usig, a, lds, s);
+    case 8: return as_host::launch_shared<8>(jpl, smax, usig, a, lds, s);
+    case 16: return as_host::launch_shared<16>(jpl, smax, usig, a, lds, s);
+    case 32: return as_host::launch_shared<32>(jpl, smax, usig, a, lds, s);
+    default: return as_host::launch_shared<64>(jpl, smax, usig, a, lds, s);
   }
 }
 
@@ -122,12 +102,13 @@ int simd_count() {
 // GPL = 1, 2, 4 are measured values.  Shapes whose LDS tables do not fit are
 // skipped (a wider W means fewer job slots per workgroup).  ALPASERVE_GPL=1|2|4
 // forces GPL.  Returns false when no shape fits.
-bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, int& GPL) {
+bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, int& GPL,
+                  bool allow_force = true) {
   const int Gp = pow2ceil(G);
   const double instr[3] = {1.0, 1.45, 2.3};
   const int n_simd = simd_count();
   int force = 0;
-  if (const char* e = getenv("ALPASERVE_GPL")) force = atoi(e);
+  if (const char* e = getenv("ALPASERVE_GPL"); e && allow_force) force = atoi(e);
   double best = 1e300;
   bool found = false;
   for (int i = 0; i < 3; ++i) {
@@ -147,44 +128,29 @@ bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, in
       break;  // the narrowest W that fits is the cheapest for this GPL
     }
   }
+  // a forced GPL that does not apply to this problem yields to the cost model
+  if (!found && force) return choose_shape(G, J, seg, M, C, smax, W, GPL, false);
   return found;
 }
 
-// ------------------------------------------------------- shared-trace path
-template <int W, int SMAX>
-hipError_t launch_shared_t(const KArgs& a, bool usig, size_t lds, hipStream_t s) {
-  constexpr int slots = (64 / W) * as_dev::kWaves;
-  const int grid = (a.J + slots - 1) / slots;
-  if (usig)
-    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, true>), dim3(grid), dim3(as_dev::kThreads), lds,
-                       s, a);
-  else
-    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, false>), dim3(grid), dim3(as_dev::kThreads), lds,
-                       s, a);
-  return hipGetLastError();
-}
-
-template <int W>
-hipError_t launch_shared_s(int smax, const KArgs& a, bool usig, size_t lds, hipStream_t s) {
-  switch (smax) {
-    case 1: return launch_shared_t<W, 1>(a, usig, lds, s);
-    case 2: return launch_shared_t<W, 2>(a, usig, lds, s);
-    case 4: return launch_shared_t<W, 4>(a, usig, lds, s);
-    default: return launch_shared_t<W, 8>(a, usig, lds, s);
+// Jobs per lane: two jobs per lane halve the wavefronts and let two
+// independent dependency chains interleave in one instruction stream; worth
+// it once there are at least two wavefronts per SIMD to merge.
+// ALPASERVE_JPL=1|2 forces the choice.
+int choose_jpl(int W, int64_t J) {
+  if (const char* e = getenv("ALPASERVE_JPL")) {
+    const int v = atoi(e);
+    if (v == 1 || v == 2) return v;
   }
+  (void)W;
+  (void)J;
+  // measured on the 8192-placement heavy trace: one job per lane with two
+  // wavefronts per SIMD (930 ms) beats two jobs per lane with one (1262 ms)
+  return 1;
 }
 
 hipError_t launch_shared(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
-  const bool usig = a.K == 1;
-  switch (W) {
-    case 1: return launch_shared_s<1>(smax, a, usig, lds, s);
-    case 2: return launch_shared_s<2>(smax, a, usig, lds, s);
-    case 4: return launch_shared_s<4>(smax, a, usig, lds, s);
-    case 8: return launch_shared_s<8>(smax, a, usig, lds, s);
-    case 16: return launch_shared_s<16>(smax, a, usig, lds, s);
-    case 32: return launch_shared_s<32>(smax, a, usig, lds, s);
-    default: return launch_shared_s<64>(smax, a, usig, lds, s);
-  }
+  return launch_shared_any(W, choose_jpl(W, a.J), smax, a.K == 1, a, lds, s);
 }
 
 // Which kernel family runs a shared-trace call: the scalar path by default;
@@ -378,7 +344,7 @@ int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
     return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
                 a.M, a.C, smax);
   const size_t lds = lds_bytes(W, smax, false, a.M, a.C);
-  hipError_t e = launch<false>(W, GPL, smax, a, lds, (hipStream_t)stream);
+  hipError_t e = launch_lds_any(W, GPL, smax, false, a, lds, (hipStream_t)stream);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -418,7 +384,7 @@ int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_o
     return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
                 a.M, a.C, smax);
   const size_t lds = lds_bytes(W, smax, true, a.M, a.C);
-  hipError_t e = launch<true>(W, GPL, smax, a, lds, (hipStream_t)stream);
+  hipError_t e = launch_lds_any(W, GPL, smax, true, a, lds, (hipStream_t)stream);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

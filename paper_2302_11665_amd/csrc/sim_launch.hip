@@ -1,0 +1,80 @@
+// Kernel launchers for one lanes-per-job width W = AS_W (see sim_launch.hpp).
+#include <hip/hip_runtime.h>
+
+#include "sim_kernel.hpp"
+#include "sim_launch.hpp"
+#include "sim_shared.hpp"
+
+#ifndef AS_W
+#error "compile with -DAS_W=<lanes per job>"
+#endif
+
+namespace as_host {
+namespace {
+
+template <int W, int GPL, int SMAX, bool SEG>
+hipError_t lds_t(const KArgs& a, size_t lds, hipStream_t s) {
+  if constexpr (W * GPL > 64) {
+    return hipErrorInvalidValue;
+  } else {
+    constexpr int slots = (64 / W) * as_dev::kWaves;
+    const int grid = (a.J + slots - 1) / slots;
+    hipLaunchKernelGGL((as_dev::sim_kernel<W, GPL, SMAX, SEG>), dim3(grid), dim3(as_dev::kThreads), lds,
+                       s, a);
+    return hipGetLastError();
+  }
+}
+
+template <int W, int GPL, bool SEG>
+hipError_t lds_s(int smax, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (smax) {
+    case 1: return lds_t<W, GPL, 1, SEG>(a, lds, s);
+    case 2: return lds_t<W, GPL, 2, SEG>(a, lds, s);
+    case 4: return lds_t<W, GPL, 4, SEG>(a, lds, s);
+    default: return lds_t<W, GPL, 8, SEG>(a, lds, s);
+  }
+}
+
+template <int W, int JPL, int SMAX>
+hipError_t shared_t(bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+  constexpr int slots = (64 / W) * JPL * as_dev::kWaves;
+  const int grid = (a.J + slots - 1) / slots;
+  if (usig)
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, JPL, SMAX, true>), dim3(grid), dim3(as_dev::kThreads),
+                       lds, s, a);
+  else
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, JPL, SMAX, false>), dim3(grid),
+                       dim3(as_dev::kThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int W, int JPL>
+hipError_t shared_s(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (smax) {
+    case 1: return shared_t<W, JPL, 1>(usig, a, lds, s);
+    case 2: return shared_t<W, JPL, 2>(usig, a, lds, s);
+    case 4: return shared_t<W, JPL, 4>(usig, a, lds, s);
+    default: return shared_t<W, JPL, 8>(usig, a, lds, s);
+  }
+}
+
+}  // namespace
+
+template <int W>
+hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (gpl) {
+    case 1: return seg ? lds_s<W, 1, true>(smax, a, lds, s) : lds_s<W, 1, false>(smax, a, lds, s);
+    case 2: return seg ? lds_s<W, 2, true>(smax, a, lds, s) : lds_s<W, 2, false>(smax, a, lds, s);
+    default: return seg ? lds_s<W, 4, true>(smax, a, lds, s) : lds_s<W, 4, false>(smax, a, lds, s);
+  }
+}
+
+template <int W>
+hipError_t launch_shared(int jpl, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+  return jpl == 2 ? shared_s<W, 2>(smax, usig, a, lds, s) : shared_s<W, 1>(smax, usig, a, lds, s);
+}
+
+template hipError_t launch_lds<AS_W>(int, int, bool, const KArgs&, size_t, hipStream_t);
+template hipError_t launch_shared<AS_W>(int, int, bool, const KArgs&, size_t, hipStream_t);
+
+}  // namespace as_host

@@ -1,0 +1,33 @@
+// Kernel launchers, one translation unit per lanes-per-job width W (the
+// build compiles sim_launch.hip once per W with -DAS_W=W and links them).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "sim_kernel.hpp"
+
+namespace as_host {
+
+using as_dev::KArgs;
+
+// General LDS-staged kernel: GPL groups per lane, SEG = per-job segments.
+template <int W>
+hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, hipStream_t s);
+
+// Shared-trace kernel: JPL jobs per lane.
+template <int W>
+hipError_t launch_shared(int jpl, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s);
+
+#define AS_DECLARE_W(W)                                                                       \
+  extern template hipError_t launch_lds<W>(int, int, bool, const KArgs&, size_t, hipStream_t); \
+  extern template hipError_t launch_shared<W>(int, int, bool, const KArgs&, size_t, hipStream_t);
+AS_DECLARE_W(1)
+AS_DECLARE_W(2)
+AS_DECLARE_W(4)
+AS_DECLARE_W(8)
+AS_DECLARE_W(16)
+AS_DECLARE_W(32)
+AS_DECLARE_W(64)
+#undef AS_DECLARE_W
+
+}  // namespace as_host

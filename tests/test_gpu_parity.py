@@ -15,14 +15,35 @@ from oracle_pins import random_case  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 
+# kernel selections the library offers (environment variables read per call):
+# the shared-trace kernel with one or two jobs per lane, and the general
+# LDS-staged kernel with one or two groups per lane
+VARIANTS = {
+    "shared": {},
+    "shared_jpl2": {"ALPASERVE_JPL": "2"},
+    "lds": {"ALPASERVE_PATH": "lds", "ALPASERVE_GPL": "1"},
+    "lds_gpl2": {"ALPASERVE_PATH": "lds", "ALPASERVE_GPL": "2"},
+}
+
+
 @pytest.fixture(scope="module")
-def gpu():
+def gpu_api():
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2302_11665_amd import api, sim
     say("library:", sim.as_version())
     return api
+
+
+@pytest.fixture(params=sorted(VARIANTS))
+def gpu(request, gpu_api, monkeypatch):
+    for k in ("ALPASERVE_JPL", "ALPASERVE_PATH", "ALPASERVE_GPL"):
+        monkeypatch.delenv(k, raising=False)
+    for k, v in VARIANTS[request.param].items():
+        monkeypatch.setenv(k, v)
+    say("variant", request.param)
+    return gpu_api
 
 
 def test_c1_all_placements(gpu):
@@ -155,7 +176,8 @@ def test_empty_trace_and_zero_jobs(gpu):
     assert np.all(res["digest"] == 0)
 
 
-def test_deterministic_repeat(gpu):
+def test_deterministic_repeat(gpu_api):
+    gpu = gpu_api
     from paper_2302_11665_amd.workload import problems
     pb = problems.c2_greedy_step(duration=120.0)
     dp = gpu.upload(pb)
@@ -168,7 +190,7 @@ def test_deterministic_repeat(gpu):
         assert a["finish"][j].tobytes() == b["finish"][j].tobytes()
 
 
-def test_validate_catches_bad_data(gpu):
+def test_validate_catches_bad_data(gpu_api):
     import torch
     from paper_2302_11665_amd import sim
     from paper_2302_11665_amd.workload import problems
