@@ -147,6 +147,53 @@ int as_validate(const as_trace_t* trace, const as_models_t* models,
                 const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
                 void* stream);
 
+/*
+ * Alg. 1 of the paper (simulator-guided greedy model selection, Sec. 4.2)
+ * with beam size 1 on one group partition.  Starting from the empty selection,
+ * every step scores each feasible addition -- a (model m, group g) pair with g
+ * not yet hosting m whose weight still fits in g's memory -- by simulating the
+ * selection plus that replica over the trace (one batched launch per step),
+ * commits the candidate with the most served requests (lowest candidate index
+ * in (m, g) order on ties), and repeats until no addition fits.  The result is
+ * the best selection seen (replaced only by a strictly better one; the empty
+ * selection serves 0).
+ *   trace, models     device data as for as_simulate_placements
+ *   weight_mib        HOST [M] model weights (integer MiB, >= 0)
+ *   n_groups          G, 1..AS_MAX_GROUPS
+ *   group_cfg         HOST [G] configuration of each group (-1 = no group)
+ *   group_mem_mib     HOST [G] memory of each group (sum of its devices', MiB):
+ *                     a selection fits iff every group's hosted weights sum to
+ *                     at most its memory (each device of a group stores 1/(S*k)
+ *                     of every hosted model)
+ *   slo_scale         one SLO multiple for every model (>= 0, +inf allowed)
+ *   best_mask         HOST out [M] bit g set <=> group g hosts model m
+ *   best_served       HOST out served requests of best_mask
+ *   step_model/_group/_served  HOST out [max_steps] trajectory (may be NULL
+ *                     when max_steps = 0); *n_steps = steps taken (steps beyond
+ *                     max_steps are taken but not recorded)
+ * Synchronous on `stream`; allocates device memory for the candidate batch.
+ */
+int as_greedy_placement(const as_trace_t* trace, const as_models_t* models,
+                        const int64_t* weight_mib, int32_t n_groups, const int32_t* group_cfg,
+                        const int64_t* group_mem_mib, double slo_scale, uint64_t* best_mask,
+                        int64_t* best_served, int32_t* step_model, int32_t* step_group,
+                        int64_t* step_served, int32_t max_steps, int32_t* n_steps,
+                        void* stream);
+
+/*
+ * Reduced Alg. 2 (Sec. 4.2): run as_greedy_placement on each of n_partitions
+ * partitions and keep the strictly best (first on ties).  Partition p has
+ * part_groups[p] groups whose configurations and memories are
+ * part_cfg[off_p ..] and part_mem_mib[off_p ..], off_p = sum of earlier
+ * part_groups (HOST arrays).  Outputs: *best_partition, best_mask[M] (HOST),
+ * *best_served, part_served[n_partitions] (HOST, each partition's best).
+ */
+int as_partition_search(const as_trace_t* trace, const as_models_t* models,
+                        const int64_t* weight_mib, int32_t n_partitions, const int32_t* part_groups,
+                        const int32_t* part_cfg, const int64_t* part_mem_mib, double slo_scale,
+                        int32_t* best_partition, uint64_t* best_mask, int64_t* best_served,
+                        int64_t* part_served, void* stream);
+
 /* Message of the last failed call on this thread ("" if none); valid until
  * the next call on this thread. */
 const char* as_last_error(void);

@@ -76,6 +76,13 @@ def lib():
         L.as_validate.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t),
                                   ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, _P]
         L.as_validate.restype = ctypes.c_int
+        L.as_greedy_placement.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t), _P,
+                                          ctypes.c_int32, _P, _P, ctypes.c_double, _P, _P, _P, _P, _P,
+                                          ctypes.c_int32, _P, _P]
+        L.as_greedy_placement.restype = ctypes.c_int
+        L.as_partition_search.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t), _P,
+                                          ctypes.c_int32, _P, _P, _P, ctypes.c_double, _P, _P, _P, _P, _P]
+        L.as_partition_search.restype = ctypes.c_int
         L.as_last_error.argtypes = []
         L.as_last_error.restype = ctypes.c_char_p
         L.as_version.argtypes = []
@@ -200,3 +207,53 @@ def u64(x) -> np.ndarray:
     if not isinstance(x, np.ndarray):
         x = x.cpu().numpy()
     return x.view(np.uint64)
+
+
+def as_greedy_placement(t, model, d_single, cfg_stages, stage_lat, weight_mib, group_cfg, group_mem_mib,
+                        slo_scale, max_steps=4096, stream=None):
+    """Marshal to as_greedy_placement (device trace/model tables, host
+    partition).  Returns dict(best_mask uint64[M], best_served, steps=[(m, g, served)])."""
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    M = md.n_models
+    w = np.ascontiguousarray(weight_mib, dtype=np.int64)
+    gc = np.ascontiguousarray(group_cfg, dtype=np.int32)
+    gm = np.ascontiguousarray(group_mem_mib, dtype=np.int64)
+    best = np.zeros(M, dtype=np.uint64)
+    best_s = np.zeros(1, dtype=np.int64)
+    sm = np.zeros(max_steps, dtype=np.int32)
+    sg = np.zeros(max_steps, dtype=np.int32)
+    ss = np.zeros(max_steps, dtype=np.int64)
+    n = np.zeros(1, dtype=np.int32)
+    rc = lib().as_greedy_placement(ctypes.byref(tr), ctypes.byref(md), w.ctypes.data, int(gc.shape[0]),
+                                   gc.ctypes.data, gm.ctypes.data, float(slo_scale), best.ctypes.data,
+                                   best_s.ctypes.data, sm.ctypes.data, sg.ctypes.data, ss.ctypes.data,
+                                   max_steps, n.ctypes.data, _stream(stream))
+    _check(rc)
+    k = min(int(n[0]), max_steps)
+    return {"best_mask": best, "best_served": int(best_s[0]), "n_steps": int(n[0]),
+            "steps": [(int(sm[i]), int(sg[i]), int(ss[i])) for i in range(k)]}
+
+
+def as_partition_search(t, model, d_single, cfg_stages, stage_lat, weight_mib, partitions, slo_scale,
+                        stream=None):
+    """Marshal to as_partition_search.  partitions: list of dicts with host
+    arrays group_cfg[G], group_mem_mib[G]."""
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    M = md.n_models
+    w = np.ascontiguousarray(weight_mib, dtype=np.int64)
+    pg = np.array([len(p["group_cfg"]) for p in partitions], dtype=np.int32)
+    pc = np.ascontiguousarray(np.concatenate([p["group_cfg"] for p in partitions]), dtype=np.int32)
+    pm = np.ascontiguousarray(np.concatenate([p["group_mem_mib"] for p in partitions]), dtype=np.int64)
+    bp = np.zeros(1, dtype=np.int32)
+    best = np.zeros(M, dtype=np.uint64)
+    bs = np.zeros(1, dtype=np.int64)
+    ps = np.zeros(len(partitions), dtype=np.int64)
+    rc = lib().as_partition_search(ctypes.byref(tr), ctypes.byref(md), w.ctypes.data, len(partitions),
+                                   pg.ctypes.data, pc.ctypes.data, pm.ctypes.data, float(slo_scale),
+                                   bp.ctypes.data, best.ctypes.data, bs.ctypes.data, ps.ctypes.data,
+                                   _stream(stream))
+    _check(rc)
+    return {"best_partition": int(bp[0]), "best_mask": best, "best_served": int(bs[0]),
+            "part_served": ps.tolist()}

@@ -263,7 +263,14 @@ def c5_sweep(group_cfg, host_mask, base: Optional[GreedyProblem] = None, n: int 
     fin = np.array([q for q, p in enumerate(idx) if p in diag], dtype=np.int32)
     gcfg = np.asarray(group_cfg, np.int32).reshape(1, -1)
     hm = np.asarray(host_mask, np.uint64).reshape(1, -1)
-    return SweepProblem("c5_sweep", t, mo.astype(np.int32), offs, base.d_single, base.cfg_stages,
-                        base.stage_lat, gcfg, hm, np.zeros(len(idx), np.int32),
+    # keep only the configurations the placement uses (renumbered in order)
+    used = sorted(set(int(c) for c in gcfg.ravel() if c >= 0))
+    remap = {c: i for i, c in enumerate(used)}
+    gcfg = np.array([[remap[int(c)] if c >= 0 else -1 for c in gcfg[0]]], np.int32)
+    cfg_stages = base.cfg_stages[used]
+    smax = int(cfg_stages.max())
+    L = np.ascontiguousarray(base.stage_lat[:, used, :smax])
+    return SweepProblem("c5_sweep", t, mo.astype(np.int32), offs, base.d_single, cfg_stages,
+                        L, gcfg, hm, np.zeros(len(idx), np.int32),
                         np.arange(len(idx), dtype=np.int32), scales, fin,
-                        {"grid": n, "points": idx})
+                        {"grid": n, "points": idx, "configs": used})

@@ -1,0 +1,136 @@
+"""GPU parity of the host drivers on top of the simulator: the native greedy
+placement search (Alg. 1, beam 1) and reduced partition search (Alg. 2)
+against the oracle's greedy, and the SLO-curve sweep (per-job trace segments)
+against the oracle, bit-exact."""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+from gpu_common import say  # noqa: E402
+
+import oracle  # noqa: E402
+from oracle import greedy as ogreedy  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2302_11665_amd import sim
+    return sim
+
+
+def _upload(sim, gp):
+    d = sim.to_device
+    return d(gp.t), d(gp.model), d(gp.d_single), d(gp.stage_lat)
+
+
+def test_greedy_trajectory_matches_oracle_reduced(dev):
+    from paper_2302_11665_amd.workload import problems
+    gp = problems.c3_greedy(duration=60.0)
+    t, m, d, L = _upload(dev, gp)
+    lib = oracle.lib()
+    for pi in (3, 6, 9):  # 16 groups (S=4), 8 groups (S=8), 8 groups (S=1, k=8)
+        part = gp.partitions[pi]
+        say("greedy partition", pi, part["label"])
+        r = dev.as_greedy_placement(t, m, d, gp.cfg_stages, L, gp.weight_mib, part["group_cfg"],
+                                    part["group_mem_mib"], gp.slo_scale)
+        o = ogreedy.greedy_selection(lib, gp.t, gp.model, gp.d_single, gp.weight_mib, gp.cfg_stages,
+                                     gp.stage_lat, part["group_cfg"], part["group_mem_mib"], gp.slo_scale)
+        assert r["n_steps"] == len(o["steps"])
+        assert r["steps"] == [tuple(int(x) for x in s) for s in o["steps"]]
+        assert r["best_served"] == o["best_served"]
+        assert [int(x) for x in r["best_mask"]] == [int(x) for x in o["best_mask"]]
+
+
+def test_partition_search_matches_oracle_small(dev):
+    from paper_2302_11665_amd.workload import problems
+    gp = problems.c3_greedy(duration=30.0, n_models=8, n_devices=16,
+                            partitions=[(2, 2, 1), (4, 4, 1), (4, 2, 2), (8, 8, 1), (16, 4, 4)])
+    t, m, d, L = _upload(dev, gp)
+    r = dev.as_partition_search(t, m, d, gp.cfg_stages, L, gp.weight_mib, gp.partitions, gp.slo_scale)
+    best, results = ogreedy.reduced_partition_search(oracle.lib(), gp.t, gp.model, gp.d_single,
+                                                     gp.weight_mib, gp.cfg_stages, gp.stage_lat,
+                                                     gp.partitions, gp.slo_scale)
+    assert r["part_served"] == [x["best_served"] for x in results]
+    assert r["best_partition"] == best["partition"]
+    assert r["best_served"] == best["best_served"]
+    assert [int(x) for x in r["best_mask"]] == [int(x) for x in best["best_mask"]]
+
+
+def test_full_greedy_search_matches_oracle_fixture(dev):
+    """The whole 10-partition greedy search of the 32-model / 64-device
+    workload (20 minutes of trace), every step's choice and served count equal
+    to the oracle's stored trajectory."""
+    from paper_2302_11665_amd.workload import problems
+    with open(os.path.join(GOLDEN, "c3_greedy_oracle.json")) as f:
+        fx = json.load(f)
+    gp = problems.c3_greedy()
+    assert len(gp.t) == fx["n_requests"]
+    t, m, d, L = _upload(dev, gp)
+    for pi, part in enumerate(gp.partitions):
+        say("full greedy partition", pi, part["label"])
+        r = dev.as_greedy_placement(t, m, d, gp.cfg_stages, L, gp.weight_mib, part["group_cfg"],
+                                    part["group_mem_mib"], gp.slo_scale)
+        want = fx["partitions"][pi]
+        assert r["steps"] == [tuple(s) for s in want["steps"]], pi
+        assert r["best_served"] == want["best_served"]
+        assert [str(int(x)) for x in r["best_mask"]] == want["best_host_mask"]
+    r = dev.as_partition_search(t, m, d, gp.cfg_stages, L, gp.weight_mib, gp.partitions, gp.slo_scale)
+    assert r["best_partition"] == fx["best_partition"]
+    assert r["best_served"] == fx["best_served"]
+
+
+def _c5_placement():
+    with open(os.path.join(GOLDEN, "c3_greedy_oracle.json")) as f:
+        fx = json.load(f)
+    return (np.array(fx["best_group_cfg"], np.int32),
+            np.array([int(x) for x in fx["best_host_mask"]], np.uint64))
+
+
+def _oracle_sweep(sp, jobs, finish):
+    lib = oracle.lib()
+    out = {}
+    for j in jobs:
+        s = int(sp.job_segment[j])
+        a, b = int(sp.seg_offsets[s]), int(sp.seg_offsets[s + 1])
+        out[j] = lib.simulate_job(sp.t[a:b], sp.model[a:b], sp.d_single, sp.cfg_stages, sp.stage_lat,
+                                  sp.group_cfg[sp.job_placement[j]], sp.host_mask[sp.job_placement[j]],
+                                  sp.job_scale[j], want_finish=j in finish)
+    return out
+
+
+def _compare_sweep(sp, res, ora):
+    lens = np.diff(sp.seg_offsets)
+    for j, (s, dg, fin) in ora.items():
+        n = int(lens[sp.job_segment[j]])
+        assert int(res["served"][j]) == s, j
+        assert tuple(int(x) for x in res["digest"][j]) == dg, j
+        assert res["attain"][j] == (s / n if n else 0.0), j
+        if fin is not None:
+            assert res["finish"][j][:n].tobytes() == fin.tobytes(), j
+
+
+def test_sweep_subset_matches_oracle(dev):
+    """48 grid points of the SLO-curve sweep (own trace each, scale per job),
+    including four diagonal points with per-request outputs."""
+    from paper_2302_11665_amd import api
+    from paper_2302_11665_amd.workload import problems
+    gcfg, hm = _c5_placement()
+    rng = np.random.default_rng(5)
+    pts = sorted(set(rng.choice(4096, 44, replace=False).tolist()) | {0, 273, 273 * 7, 4095})
+    sp = problems.c5_sweep(gcfg, hm, points=pts)
+    say("sweep subset", len(pts), "jobs", len(sp.t), "requests")
+    ds = api.upload_sweep(sp)
+    api.run_sweep(ds)
+    res = api.sweep_results(ds)
+    fins = set(int(x) for x in sp.finish_jobs)
+    _compare_sweep(sp, res, _oracle_sweep(sp, range(len(pts)), fins))

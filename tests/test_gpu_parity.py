@@ -219,3 +219,18 @@ def test_validate_catches_bad_data(gpu_api):
     with pytest.raises(sim.SimError):
         sim.as_validate(*a2)
     torch.cuda.synchronize()
+
+
+def test_c4_full_size_sampled(gpu_api):
+    """The benchmark workload at full size (8192 placements x 3.6 M requests) in
+    the benchmark's launch configuration; the oracle recomputes a sample of
+    jobs and two of the per-request output rows."""
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c4_heavy()
+    say("c4 full", pb.n_jobs, len(pb.t))
+    res = gpu_api.simulate_problem(pb)
+    rng = np.random.default_rng(44)
+    jobs = sorted(set(rng.choice(pb.n_jobs, 6, replace=False).tolist()) | {int(pb.finish_jobs[0]),
+                                                                           int(pb.finish_jobs[-1])})
+    fins = [int(pb.finish_jobs[0]), int(pb.finish_jobs[-1])]
+    compare(res, oracle_problem(pb, jobs=jobs, finish_jobs=fins), len(pb.t), "c4 full sampled")
