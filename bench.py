@@ -30,6 +30,23 @@ METRIC = "simulated request×placement events/sec on 1 GPU; % of HBM/VALU roofli
 PEAK_FP64_OPS = 256 * 4 * 16 * 2.4e9
 HBM_PEAK = 8.0e12
 
+# HBM traffic of one launch of the simulator kernel on the default workload:
+# rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by
+# what the same counter reads for a plain 1 GiB device copy (FETCH_SIZE reads
+# 524299.5 KiB for 1048576 KiB fetched, WRITE_SIZE exactly 1048576 KiB).  The
+# figures belong to the kernel sources whose SHA-256 is recorded here; once
+# those change, traffic is reported as null until it is measured again.
+KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd/csrc/sim_kernel.hpp",
+                  "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
+                  "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/build.py",
+                  "include/alpaserve_sim.h"]
+MEASURED_TRAFFIC = {
+    "sources_sha256": "43a1895b37ca96cf09c326d8087a0ebc0341018640f2e0a702aed10de6515145",
+    "kernel": "shared_kernel<16, 1, 4, true>",
+    "fetch_kib": 349747.0625, "write_kib": 450111.0,
+    "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1.0,
+}
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -54,6 +71,32 @@ def algorithmic_ops(pb):
     return ops_per_scale * pb.slo_scale.shape[0]
 
 
+def sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(KERNEL_SOURCES):
+        h.update(os.path.basename(f).encode())
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(default_workload):
+    m = MEASURED_TRAFFIC
+    if not default_workload or sources_sha256() != m["sources_sha256"]:
+        return None
+    return round((m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024.0)
+
+
+def algorithmic_bytes(pb):
+    """Bytes the definition moves per launch: the trace read once (time f64 +
+    model i32), the placement tables, the per-job outputs (served i64, attain
+    f64, digest 2 x u64) and the per-request outputs of the selected jobs."""
+    N, J = len(pb.t), pb.n_jobs
+    return (12 * N + pb.group_cfg.nbytes + pb.host_mask.nbytes + pb.stage_lat.nbytes
+            + J * (8 + 8 + 16) + 8 * N * len(pb.finish_jobs))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -61,7 +104,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--placements", type=int, default=8192)
     ap.add_argument("--duration", type=float, default=3600.0)
-    ap.add_argument("--cpu-sample", type=int, default=64, help="jobs timed on the CPU oracle")
+    ap.add_argument("--cpu-sample", type=int, default=192, help="jobs timed on the CPU oracle")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
                     help="instead of the benchmark, run a plain device copy of this many GiB "
@@ -124,7 +167,9 @@ def main():
     achieved = ops / (ms / 1000.0) / 1e12
     peak = PEAK_FP64_OPS / 1e12
     roof = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(peak, 2), "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 5), "traffic": None,
+            "frac": round(achieved / peak, 5),
+            "traffic": measured_traffic(args.placements == 8192 and args.duration == 3600.0),
+            "algorithmic_bytes": int(algorithmic_bytes(pb)),
             "ops_per_event": round(ops / events, 3),
             "note": "fp64 lane-ops (max/add/cmp/mul, no FMA) of the definition per launch / mean launch time"}
 
