@@ -12,7 +12,13 @@ Prints ONE JSON line: events/s (request x placement pairs per second), the
 roofline of the simulator kernel, and the CPU oracle's rate on a bounded
 sample of the same workload (single thread), with sampled bit-exact parity.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu]
+Also reported, as "sweep": the SLO-curve sweep workload -- one fixed
+placement (the 32-model / 64-device greedy search's best, 64 single-device
+groups) over a 16 x 16 x 16 grid of rate scale, CV and SLO scale, every grid
+point with its own 10-minute trace (4096 segments, about 4.4e8 requests) --
+timed the same way, with its HBM roofline (each segment is read once).
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep]
 """
 import argparse
 import json
@@ -97,6 +103,64 @@ def algorithmic_bytes(pb):
             + J * (8 + 8 + 16) + 8 * N * len(pb.finish_jobs))
 
 
+def sweep_placement():
+    """The best placement of the 32-model / 64-device greedy search, stored
+    with the search's result (inputs only: group configurations and hosting
+    masks)."""
+    import numpy as np
+    with open(os.path.join(ROOT, "tests", "golden", "c3_greedy_oracle.json")) as f:
+        fx = json.load(f)
+    return (np.array(fx["best_group_cfg"], np.int32),
+            np.array([int(x) for x in fx["best_host_mask"]], np.uint64))
+
+
+def sweep_algorithmic_bytes(sp, n_finish_rows, stride):
+    """Every segment read once (12 B per request), offsets and job records,
+    per-job outputs and the per-request outputs of the selected jobs."""
+    return (12 * len(sp.t) + sp.seg_offsets.nbytes + 16 * len(sp.job_segment)
+            + 32 * len(sp.job_segment) + 8 * n_finish_rows * stride)
+
+
+def bench_sweep(args, np, torch, api, problems):
+    t0 = time.time()
+    gcfg, hm = sweep_placement()
+    sp = problems.c5_sweep(gcfg, hm)
+    gen_s = time.time() - t0
+    events = sp.events
+    log(f"sweep: {len(sp.job_segment)} jobs, {events:.3e} events; built in {gen_s:.2f}s")
+    t0 = time.time()
+    ds = api.upload_sweep(sp)
+    torch.cuda.synchronize()
+    up_s = time.time() - t0
+    for _ in range(args.warmup):
+        api.run_sweep(ds)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev[0].record(stream)
+    for k in range(args.steps):
+        api.run_sweep(ds)
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
+    ms = float(np.mean(per))
+    log(f"sweep: {ms:.3f} ms/step (min {min(per):.3f}, max {max(per):.3f})")
+    nbytes = sweep_algorithmic_bytes(sp, len(ds.finish_jobs), ds.finish_stride)
+    gbs = nbytes / (ms / 1000.0) / 1e9
+    res = api.sweep_results(ds)
+    del ds
+    torch.cuda.empty_cache()
+    return {"workload": "SLO-curve sweep: 32 models, 64 single-device groups (greedy best), 16x16x16 grid of "
+                        "rate scale x CV x SLO scale, own 600 s trace per point",
+            "jobs": int(len(sp.job_segment)), "requests": int(len(sp.t)), "events": int(events),
+            "ms_per_step": round(ms, 3), "value": round(events / (ms / 1000.0), 1), "unit": "events/s",
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                         "frac": round(gbs * 1e9 / HBM_PEAK, 5), "traffic": None,
+                         "algorithmic_bytes": int(nbytes)},
+            "served_total": int(res["served"].sum()),
+            "trace_gen_s": round(gen_s, 3), "upload_s": round(up_s, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -106,6 +170,9 @@ def main():
     ap.add_argument("--duration", type=float, default=3600.0)
     ap.add_argument("--cpu-sample", type=int, default=192, help="jobs timed on the CPU oracle")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the SLO-curve sweep workload")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="time only the SLO-curve sweep (prints its object alone)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
                     help="instead of the benchmark, run a plain device copy of this many GiB "
                          "(HBM counter calibration)")
@@ -130,6 +197,10 @@ def main():
 
     from paper_2302_11665_amd import api, sim
     from paper_2302_11665_amd.workload import problems
+
+    if args.sweep_only:
+        print(json.dumps({"sweep": bench_sweep(args, np, torch, api, problems)}), flush=True)
+        return
 
     t0 = time.time()
     pb = problems.c4_heavy(duration=args.duration, n_placements=args.placements)
@@ -212,6 +283,10 @@ def main():
                                          f"{len(sample) * N:.3e} events, single thread, {cpu_s:.1f}s"}
         out["parity_sampled"] = {"jobs": len(sample), "finish_rows": len(fset), "mismatches": mism}
         out["speedup_vs_cpu_oracle"] = round(value / cpu_rate, 1)
+    if not args.no_sweep:
+        del dp
+        torch.cuda.empty_cache()
+        out["sweep"] = bench_sweep(args, np, torch, api, problems)
     print(json.dumps(out), flush=True)
 
 

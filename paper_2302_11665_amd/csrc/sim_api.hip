@@ -12,6 +12,7 @@
 
 #include "alpaserve_sim.h"
 #include "sim_kernel.hpp"
+#include "sim_shared.hpp"
 #include "sim_launch.hpp"
 
 namespace {
@@ -56,6 +57,21 @@ size_t lds_bytes(int W, int SMAX, bool seg, int M, int C) {
 
 constexpr size_t kMaxLds = 64 * 1024;
 
+// LDS a workgroup of the shared-trace kernel may use: the device's per-block
+// limit (160 KiB on gfx950), cached per device.
+size_t shared_lds_limit() {
+  static size_t cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kMaxLds;
+  if (cache[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
+      v = (int)kMaxLds;
+    cache[dev] = (size_t)(v > 160 * 1024 ? 160 * 1024 : v);
+  }
+  return cache[dev];
+}
+
 
 hipError_t launch_lds_any(int W, int gpl, int smax, bool seg, const KArgs& a, size_t lds, hipStream_t s) {
   switch (W) {
@@ -69,16 +85,15 @@ hipError_t launch_lds_any(int W, int gpl, int smax, bool seg, const KArgs& a, si
   }
 }
 
-hipError_t launch_shared_any(int W, int jpl, int smax, bool usig, const KArgs& a, size_t lds,
-                             hipStream_t s) {
+hipError_t launch_shared_any(int W, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
   switch (W) {
-    case 1: return as_host::launch_shared<1>(jpl, smax, usig, a, lds, s);
-    case 2: return as_host::launch_shared<2>(jpl, smax, usig, a, lds, s);
-    case 4: return as_host::launch_shared<4>(jpl, smax, usig, a, lds, s);
-    case 8: return as_host::launch_shared<8>(jpl, smax, usig, a, lds, s);
-    case 16: return as_host::launch_shared<16>(jpl, smax, usig, a, lds, s);
-    case 32: return as_host::launch_shared<32>(jpl, smax, usig, a, lds, s);
-    default: return as_host::launch_shared<64>(jpl, smax, usig, a, lds, s);
+    case 1: return as_host::launch_shared<1>(smax, usig, a, lds, s);
+    case 2: return as_host::launch_shared<2>(smax, usig, a, lds, s);
+    case 4: return as_host::launch_shared<4>(smax, usig, a, lds, s);
+    case 8: return as_host::launch_shared<8>(smax, usig, a, lds, s);
+    case 16: return as_host::launch_shared<16>(smax, usig, a, lds, s);
+    case 32: return as_host::launch_shared<32>(smax, usig, a, lds, s);
+    default: return as_host::launch_shared<64>(smax, usig, a, lds, s);
   }
 }
 
@@ -132,26 +147,6 @@ bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, in
   // a forced GPL that does not apply to this problem yields to the cost model
   if (!found && force) return choose_shape(G, J, seg, M, C, smax, W, GPL, false);
   return found;
-}
-
-// Jobs per lane: two jobs per lane halve the wavefronts and let two
-// independent dependency chains interleave in one instruction stream; worth
-// it once there are at least two wavefronts per SIMD to merge.
-// ALPASERVE_JPL=1|2 forces the choice.
-int choose_jpl(int W, int64_t J) {
-  if (const char* e = getenv("ALPASERVE_JPL")) {
-    const int v = atoi(e);
-    if (v == 1 || v == 2) return v;
-  }
-  (void)W;
-  (void)J;
-  // measured on the 8192-placement heavy trace: one job per lane with two
-  // wavefronts per SIMD (930 ms) beats two jobs per lane with one (1262 ms)
-  return 1;
-}
-
-hipError_t launch_shared(int W, int smax, const KArgs& a, size_t lds, hipStream_t s) {
-  return launch_shared_any(W, choose_jpl(W, a.J), smax, a.K == 1, a, lds, s);
 }
 
 // Which kernel family runs a shared-trace call: the scalar path by default;
@@ -292,15 +287,13 @@ __global__ void validate_kernel(const double* t, const int32_t* model, int64_t n
 // kernel shape).  W is the group count on entry.
 int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
   const int64_t J = a.J;
-  if (use_shared_path()) {
-    // one group per lane; the narrowest W whose tables fit in LDS
-    int Ws = pow2ceil(a.G);
-    while (Ws < 64 && lds_bytes(Ws, smax, false, a.M, a.C) > kMaxLds) Ws *= 2;
-    const size_t lds = lds_bytes(Ws, smax, false, a.M, a.C);
-    if (lds > kMaxLds)
-      return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
-                  a.M, a.C, smax);
-    hipError_t e = launch_shared(Ws, smax, a, lds, stream);
+  // shared-trace kernel (one group per lane, W = G rounded up to a power of
+  // two) unless its tables exceed the LDS of a workgroup; then the general
+  // kernel, whose tables are smaller
+  const size_t lds_shared = as_dev::shared_lds_bytes(a.M, pow2ceil(a.C), smax);
+  if (use_shared_path() && lds_shared <= shared_lds_limit()) {
+    const int Ws = pow2ceil(a.G);
+    hipError_t e = launch_shared_any(Ws, smax, a.K == 1, a, lds_shared, stream);
     if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
   }

@@ -35,27 +35,17 @@ hipError_t lds_s(int smax, const KArgs& a, size_t lds, hipStream_t s) {
   }
 }
 
-template <int W, int JPL, int SMAX>
+template <int W, int SMAX>
 hipError_t shared_t(bool usig, const KArgs& a, size_t lds, hipStream_t s) {
-  constexpr int slots = (64 / W) * JPL * as_dev::kWaves;
+  constexpr int slots = (64 / W) * as_dev::kWaves;
   const int grid = (a.J + slots - 1) / slots;
   if (usig)
-    hipLaunchKernelGGL((as_dev::shared_kernel<W, JPL, SMAX, true>), dim3(grid), dim3(as_dev::kThreads),
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, true>), dim3(grid), dim3(as_dev::kThreads),
                        lds, s, a);
   else
-    hipLaunchKernelGGL((as_dev::shared_kernel<W, JPL, SMAX, false>), dim3(grid),
-                       dim3(as_dev::kThreads), lds, s, a);
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, false>), dim3(grid), dim3(as_dev::kThreads),
+                       lds, s, a);
   return hipGetLastError();
-}
-
-template <int W, int JPL>
-hipError_t shared_s(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
-  switch (smax) {
-    case 1: return shared_t<W, JPL, 1>(usig, a, lds, s);
-    case 2: return shared_t<W, JPL, 2>(usig, a, lds, s);
-    case 4: return shared_t<W, JPL, 4>(usig, a, lds, s);
-    default: return shared_t<W, JPL, 8>(usig, a, lds, s);
-  }
 }
 
 }  // namespace
@@ -70,11 +60,16 @@ hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, h
 }
 
 template <int W>
-hipError_t launch_shared(int jpl, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
-  return jpl == 2 ? shared_s<W, 2>(smax, usig, a, lds, s) : shared_s<W, 1>(smax, usig, a, lds, s);
+hipError_t launch_shared(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+  switch (smax) {
+    case 1: return shared_t<W, 1>(usig, a, lds, s);
+    case 2: return shared_t<W, 2>(usig, a, lds, s);
+    case 4: return shared_t<W, 4>(usig, a, lds, s);
+    default: return shared_t<W, 8>(usig, a, lds, s);
+  }
 }
 
 template hipError_t launch_lds<AS_W>(int, int, bool, const KArgs&, size_t, hipStream_t);
-template hipError_t launch_shared<AS_W>(int, int, bool, const KArgs&, size_t, hipStream_t);
+template hipError_t launch_shared<AS_W>(int, bool, const KArgs&, size_t, hipStream_t);
 
 }  // namespace as_host

@@ -14,13 +14,13 @@ using as_dev::KArgs;
 template <int W>
 hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, hipStream_t s);
 
-// Shared-trace kernel: JPL jobs per lane.
+// Shared-trace kernel: one group per lane, USIG = one SLO scale for all jobs.
 template <int W>
-hipError_t launch_shared(int jpl, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s);
+hipError_t launch_shared(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s);
 
 #define AS_DECLARE_W(W)                                                                       \
   extern template hipError_t launch_lds<W>(int, int, bool, const KArgs&, size_t, hipStream_t); \
-  extern template hipError_t launch_shared<W>(int, int, bool, const KArgs&, size_t, hipStream_t);
+  extern template hipError_t launch_shared<W>(int, bool, const KArgs&, size_t, hipStream_t);
 AS_DECLARE_W(1)
 AS_DECLARE_W(2)
 AS_DECLARE_W(4)

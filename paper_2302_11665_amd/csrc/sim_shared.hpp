@@ -1,26 +1,35 @@
 // Shared-trace serving-simulator kernel for gfx950: every job of a launch
 // simulates the same arrival trace.
 //
-// Layout as in sim_kernel.hpp with one group per lane: a job owns W lanes of a
-// wavefront, lane r of the job holds group r's stage free times in registers;
-// 64 / W jobs per wavefront, four wavefronts per workgroup.  The trace is
-// staged through LDS in chunks read with coalesced loads by the whole
-// workgroup (each request is read from HBM/L2 once per workgroup), together
-// with the stage-latency table and the SLO (or single-device latency) table.
+// Layout: a job owns W lanes of a wavefront, lane r of the job holds group r's
+// stage free times F[0..SMAX-1] in registers; 64 / W jobs per wavefront, four
+// wavefronts per workgroup.  The trace is staged through LDS in chunks read
+// with coalesced loads by the whole workgroup (each request is read from
+// HBM/L2 once per workgroup); every wavefront then reads the same words.
 //
-// Per request, lane sets are kept as 64-bit wavefront masks in scalar
-// registers: the hosting lanes come from a vector compare, the dispatch
-// target of every job is one mask, and the accepted lanes are that mask ANDed
-// with the deadline compare.  Commit and counting run under that mask.
+// Per-wavefront model records (LDS, one per model m, built when the kernel
+// starts): the wavefront's hosting lane mask for m (bit l = lane l's group
+// hosts m), the SLO (scale * d_single[m], one scale per launch) or
+// d_single[m], a count that is 0 when no job of the wavefront has two groups
+// hosting m and otherwise the number of jobs of the wavefront hosting m, and,
+// when every group of the wavefront has the same configuration, that
+// configuration's stage latencies of m.  A request therefore costs one
+// address computation and reads at immediate offsets of one record.
 //
-// Dispatch (Sec. 4.3): a per-wavefront bit per model, computed once, says
-// whether every job of the wavefront has at most one group hosting the model;
-// then the hosting lanes are the dispatch targets and no reduction is needed.
-// Otherwise the keys (stage-0 free time of hosting groups, +inf elsewhere) go
-// through the butterfly min of sim_kernel.hpp, and the lowest lane of each job
+// Dispatch (Sec. 4.3): the target of a job is the hosting lane with the
+// smallest stage-0 free time, the lowest such lane on ties.  When the record's
+// count is 0, the hosting lanes are the targets.  Otherwise the minimum is
+// found on the free times' IEEE bit patterns: free times are >= 0, so with the
+// sign bit cleared (-0 and +0 become equal) the unsigned order of the 64-bit
+// patterns is the numeric order.  The high words are reduced first with
+// one-instruction DPP min steps (v_min_u32 with a DPP operand inside 16-lane
+// rows, permlane swaps across rows).  If the hosting lanes holding the
+// minimal high word are exactly one per hosting job (their population count
+// equals the record's count), they are the targets.  Otherwise the low words
+// of the tied lanes are reduced as well, and the lowest lane of each job
 // holding the minimum -- the lowest set bit of every W-bit field of the
 // equality mask, computed on the scalar unit -- is the target.  Projection,
-// admission, commit and counting are sim_kernel.hpp's, so the results are
+// admission and counting are sim_kernel.hpp's, so the results are
 // bit-identical.
 #pragma once
 
@@ -55,97 +64,117 @@ __device__ __forceinline__ uint64_t lowest_per_field(uint64_t b) {
   }
 }
 
-// Per-lane state: group (lane mod W) of JPL different jobs.
-template <int JPL, int SMAX>
+__device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
+// Unsigned minimum over each aligned W-lane segment, in every lane of it.
+// Inside a 16-lane row each step is one v_min_u32 with a DPP operand; the
+// 16- and 32-lane steps swap rows / halves with v_permlane16/32_swap (both
+// outputs of the swap are the two halves of the butterfly).
+template <int W>
+__device__ __forceinline__ uint32_t seg_min_u32(uint32_t x) {
+  if constexpr (W >= 2) x = umin32(x, dpp_u32<kXor1>(x));
+  if constexpr (W >= 4) x = umin32(x, dpp_u32<kXor2>(x));
+  if constexpr (W >= 8) x = umin32(x, dpp_u32<kHalfMirror>(x));
+  if constexpr (W >= 16) x = umin32(x, dpp_u32<kMirror>(x));
+  if constexpr (W >= 32) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    x = umin32(r[0], r[1]);
+  }
+  if constexpr (W >= 64) {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    x = umin32(r[0], r[1]);
+  }
+  return x;
+}
+
+// Bytes of one model record: hosting mask (8), SLO or d_single (8), count
+// (4), padding (12), stage latencies (8 * SMAX); a power of two.
+template <int SMAX>
+constexpr int rec_shift() {
+  return SMAX <= 4 ? 6 : 7;
+}
+constexpr int kRecMask = 0, kRecSlo = 8, kRecCount = 16, kRecLat = 32;
+
+// Per-lane state: group (lane mod W) of one job.
+template <int SMAX>
 struct SharedLane {
-  double F[JPL][SMAX];
-  uint64_t fin_sum[JPL], hash[JPL], served[JPL];
-  uint32_t wlo[JPL];
+  double F[SMAX];
+  uint64_t fin_sum, hash, served;
+  uint32_t wlo;
 };
 
-template <int JPL>
 struct SharedConst {
-  uint64_t hostbits[JPL];  // bit m: this lane's group of job set j hosts model m
-  uint64_t single;         // bit m: no job of the wavefront has two groups hosting m
-  uint64_t segmask;        // lanes of this lane's jobs
-  const double* lrow[JPL]; // stage-latency row of job set j's configuration for model 0
-  int lshift;              // log2 of the per-model row stride (bytes) of the LDS table
-  const double* slo;       // LDS: scale * d_single[m] (one scale) or d_single[m]
-  double sigma[JPL];       // each job's scale (used when jobs differ in scale)
+  const unsigned char* rec;  // this wavefront's model records (LDS)
+  const double* lrow;        // stage-latency row of this lane's configuration for model 0 (LDS)
+  int lshift;                // log2 of the per-model row stride (bytes) of that table
+  double sigma;              // this job's scale (used when jobs differ in scale)
+  uint64_t segmask;          // lanes of this lane's job
   int seg_lane;
-  int frow[JPL];
+  int frow;                  // per-request output row of this job, -1 if none
 };
 
-// One request at trace position i for the JPL jobs of every lane.  USIG:
-// every job uses the same scale and c.slo holds the SLOs.  The JPL jobs share
-// the request inputs and their dependency chains interleave.
-template <int W, int JPL, int SMAX, bool USIG, bool FINISH>
-__device__ __forceinline__ void fast_step(SharedLane<JPL, SMAX>& st, const SharedConst<JPL>& c,
-                                          double ti, int mi, const double (&L)[JPL][SMAX],
-                                          double slo_or_d,
-                                          int64_t i, int64_t n, double* __restrict__ out_finish,
-                                          uint32_t (&sr)[JPL]) {
-  const double kInf = __builtin_inf();
-  const int mu = __builtin_amdgcn_readfirstlane(mi);
-  bool hosted[JPL];
-  uint64_t cm[JPL];  // the dispatch target of every job: one lane per job or none
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) {
-    hosted[j] = (c.hostbits[j] >> mi) & 1u;
-    cm[j] = __builtin_amdgcn_ballot_w64(hosted[j]);
-  }
-  if (!((c.single >> mu) & 1u)) {
-#pragma unroll
-    for (int j = 0; j < JPL; ++j) {
-      const double key = hosted[j] ? st.F[j][0] : kInf;
-      const double mn = seg_min<W>(key);
-      // mn == +inf: no group of the job hosts the model, so no lane matches
-      const bool eq = key == vmin(mn, 1.7976931348623157e308);
-      cm[j] = lowest_per_field<W>(__builtin_amdgcn_ballot_w64(eq));
+// One request at trace position i.  hm: the wavefront's hosting lanes; cnt:
+// the record's count; L: this lane's stage latencies of the model; sv: the
+// SLO (USIG) or d_single of the model.
+template <int W, int SMAX, bool USIG, bool FINISH>
+__device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedConst& c, double ti,
+                                          uint64_t hm, uint32_t cnt, const double (&L)[SMAX],
+                                          double sv, int64_t i, int64_t n,
+                                          double* __restrict__ out_finish, uint32_t& sr) {
+  uint64_t cm = hm;  // the dispatch target of every job: one lane per job or none
+  if (cnt != 0) {
+    const bool hosted = __builtin_amdgcn_inverse_ballot_w64(hm);
+    const uint64_t kb = (uint64_t)__double_as_longlong(st.F[0]);
+    const uint32_t khi = hosted ? ((uint32_t)(kb >> 32) & 0x7fffffffu) : 0xffffffffu;
+    const uint32_t mhi = seg_min_u32<W>(khi);
+    const uint64_t eqhi = __builtin_amdgcn_ballot_w64(khi == mhi) & hm;
+    cm = eqhi;
+    if ((uint32_t)__builtin_popcountll(eqhi) != cnt) {
+      // some job has two hosting lanes with the same high word: compare the
+      // low words of the tied lanes
+      const bool tied = __builtin_amdgcn_inverse_ballot_w64(eqhi);
+      const uint32_t klo = tied ? (uint32_t)kb : 0xffffffffu;
+      const uint32_t mlo = seg_min_u32<W>(klo);
+      cm = lowest_per_field<W>(__builtin_amdgcn_ballot_w64(klo == mlo) & eqhi);
     }
   }
-  double fs[JPL][SMAX];
-  double f[JPL];
+  // projection through this lane's stage chain (Sec. 3.4)
+  double fs[SMAX];
+  double f = ti;
 #pragma unroll
-  for (int j = 0; j < JPL; ++j) f[j] = ti;
+  for (int s = 0; s < SMAX; ++s) {
+    fs[s] = vmax(f, st.F[s]) + L[s];
+    f = fs[s];
+  }
+  // admission (Sec. 4.3, Sec. 3.2) and commit on the target lane
+  const double deadline = ti + (USIG ? sv : c.sigma * sv);
+  const uint64_t am = cm & __builtin_amdgcn_ballot_w64(!(f > deadline));
+  const bool acc = __builtin_amdgcn_inverse_ballot_w64(am);
 #pragma unroll
-  for (int s = 0; s < SMAX; ++s)
-#pragma unroll
-    for (int j = 0; j < JPL; ++j) {
-      fs[j][s] = vmax(f[j], st.F[j][s]) + L[j][s];
-      f[j] = fs[j][s];
-    }
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) {
-    const double deadline = ti + (USIG ? slo_or_d : c.sigma[j] * slo_or_d);
-    const uint64_t am = cm[j] & __builtin_amdgcn_ballot_w64(!(f[j] > deadline));
-    const bool acc = __builtin_amdgcn_inverse_ballot_w64(am);
-    if (acc) {
-#pragma unroll
-      for (int s = 0; s < SMAX; ++s) st.F[j][s] = fs[j][s];
-      st.fin_sum[j] += (uint64_t)__double_as_longlong(f[j]);
-    }
-    sr[j] = (sr[j] << 1) | (acc ? 1u : 0u);
-    if constexpr (FINISH) {
-      if (c.frow[j] >= 0) {
-        double* dst = out_finish + (int64_t)c.frow[j] * n + i;
-        if (__builtin_amdgcn_inverse_ballot_w64(cm[j])) *dst = acc ? f[j] : -1.0;
-        else if ((cm[j] & c.segmask) == 0 && c.seg_lane == 0) *dst = -2.0;
-      }
+  for (int s = 0; s < SMAX; ++s) st.F[s] = acc ? fs[s] : st.F[s];
+  st.fin_sum += acc ? (uint64_t)__double_as_longlong(f) : 0ull;
+  sr = (sr << 1) | (acc ? 1u : 0u);
+  if constexpr (FINISH) {
+    if (c.frow >= 0) {
+      double* dst = out_finish + (int64_t)c.frow * n + i;
+      if (__builtin_amdgcn_inverse_ballot_w64(cm)) *dst = acc ? f : -1.0;
+      else if ((cm & c.segmask) == 0 && c.seg_lane == 0) *dst = -2.0;
     }
   }
 }
 
 // Requests [i0, i0 + B) from the LDS chunk: read all of their inputs first
-// (LDS reads in flight together), then run them in order.  LSH: the JPL job
-// sets of every lane use the same configuration, so one stage-latency row
-// serves them all.
-template <int W, int JPL, int SMAX, int B, bool USIG, bool FINISH, bool LSH>
-__device__ __forceinline__ void fast_batch(SharedLane<JPL, SMAX>& st, const SharedConst<JPL>& c,
+// (LDS reads in flight together), then run them in order.  UNI: every group
+// of the wavefront has the same configuration, whose stage latencies the
+// model records hold; otherwise each lane reads its configuration's row.
+template <int W, int SMAX, int B, bool USIG, bool FINISH, bool UNI>
+__device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedConst& c,
                                            const double* __restrict__ cT,
                                            const int32_t* __restrict__ cM, int64_t i0, int64_t n,
-                                           double* __restrict__ out_finish, uint32_t (&sr)[JPL]) {
-  double t[B], so[B], L[B][JPL][SMAX];
+                                           double* __restrict__ out_finish, uint32_t& sr) {
+  double t[B], sv[B], L[B][SMAX];
+  uint64_t hmv[B];
+  uint32_t cnv[B];
   int m[B];
 #pragma unroll
   for (int k = 0; k < B; ++k) {
@@ -154,155 +183,127 @@ __device__ __forceinline__ void fast_batch(SharedLane<JPL, SMAX>& st, const Shar
   }
 #pragma unroll
   for (int k = 0; k < B; ++k) {
+    const unsigned char* r = c.rec + ((unsigned)m[k] << rec_shift<SMAX>());
+    hmv[k] = *(const uint64_t*)(r + kRecMask);
+    sv[k] = *(const double*)(r + kRecSlo);
+    cnv[k] = *(const uint32_t*)(r + kRecCount);
+    const double* lr = UNI ? (const double*)(r + kRecLat)
+                           : (const double*)((const char*)c.lrow + ((unsigned)m[k] << c.lshift));
 #pragma unroll
-    for (int j = 0; j < JPL; ++j) {
-      if (LSH && j > 0) {
-#pragma unroll
-        for (int s = 0; s < SMAX; ++s) L[k][j][s] = L[k][0][s];
-      } else {
-        const double* row =
-            (const double*)((const char*)c.lrow[j] + ((unsigned)m[k] << c.lshift));
-#pragma unroll
-        for (int s = 0; s < SMAX; ++s) L[k][j][s] = row[s];
-      }
-    }
-    so[k] = c.slo[m[k]];
+    for (int s = 0; s < SMAX; ++s) L[k][s] = lr[s];
   }
 #pragma unroll
-  for (int k = 0; k < B; ++k)
-    fast_step<W, JPL, SMAX, USIG, FINISH>(st, c, t[k], m[k], L[k], so[k], i0 + k, n, out_finish,
-                                          sr);
+  for (int k = 0; k < B; ++k) {
+    // record words are the same in every lane: move them to scalar registers
+    const uint64_t hm = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(hmv[k] >> 32)) << 32) |
+                        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)hmv[k]);
+    const uint32_t cnt = (uint32_t)__builtin_amdgcn_readfirstlane((int)cnv[k]);
+    fast_step<W, SMAX, USIG, FINISH>(st, c, t[k], hm, cnt, L[k], sv[k], i0 + k, n, out_finish, sr);
+  }
 }
 
 // All requests of one LDS chunk [base, base + cnt): 32-request halves of
 // 64-request accept words.
-template <int W, int JPL, int SMAX, bool USIG, bool FINISH, bool LSH>
-__device__ __forceinline__ void fast_chunk(SharedLane<JPL, SMAX>& st, const SharedConst<JPL>& c,
+template <int W, int SMAX, bool USIG, bool FINISH, bool UNI>
+__device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedConst& c,
                                            const double* __restrict__ cT,
                                            const int32_t* __restrict__ cM, int cnt, int64_t base,
                                            int64_t n, double* __restrict__ out_finish) {
-  constexpr int B = (SMAX <= 4 && JPL == 1) ? 4 : 2;
+  constexpr int B = SMAX <= 4 ? 4 : 2;
   for (int h = 0; h < cnt; h += 32) {
     const int hc = (cnt - h) < 32 ? (cnt - h) : 32;
-    uint32_t sr[JPL];
-#pragma unroll
-    for (int j = 0; j < JPL; ++j) sr[j] = 0;
+    uint32_t sr = 0;
     if (hc == 32) {
       for (int e = 0; e < 32; e += B)
-        fast_batch<W, JPL, SMAX, B, USIG, FINISH, LSH>(st, c, cT + h + e, cM + h + e, base + h + e,
-                                                       n, out_finish, sr);
+        fast_batch<W, SMAX, B, USIG, FINISH, UNI>(st, c, cT + h + e, cM + h + e, base + h + e, n,
+                                                  out_finish, sr);
     } else {
       for (int e = 0; e < hc; ++e)
-        fast_batch<W, JPL, SMAX, 1, USIG, FINISH, LSH>(st, c, cT + h + e, cM + h + e, base + h + e,
-                                                       n, out_finish, sr);
+        fast_batch<W, SMAX, 1, USIG, FINISH, UNI>(st, c, cT + h + e, cM + h + e, base + h + e, n,
+                                                  out_finish, sr);
     }
     const int64_t pos = (base + h) & 63;  // 0 or 32
     const bool end = base + h + hc == n;
-#pragma unroll
-    for (int j = 0; j < JPL; ++j) {
-      // sr holds request e at bit hc-1-e; bits: request e at bit e
-      const uint32_t bits = hc == 32 ? __builtin_bitreverse32(sr[j])
-                                     : (__builtin_bitreverse32(sr[j]) >> (32 - hc));
-      if (pos == 0 && !end) {
-        st.wlo[j] = bits;
-      } else {
-        const uint64_t w = pos == 0 ? (uint64_t)bits : (((uint64_t)bits << 32) | st.wlo[j]);
-        const uint64_t wj = seg_or<W>(w);
-        st.hash[j] = (st.hash[j] ^ wj) * kHashMul;
-        st.served[j] += (uint64_t)__popcll(wj);
-        st.wlo[j] = 0;
-      }
+    // sr holds request e at bit hc-1-e; bits: request e at bit e
+    const uint32_t bits =
+        hc == 32 ? __builtin_bitreverse32(sr) : (__builtin_bitreverse32(sr) >> (32 - hc));
+    if (pos == 0 && !end) {
+      st.wlo = bits;
+    } else {
+      const uint64_t w = pos == 0 ? (uint64_t)bits : (((uint64_t)bits << 32) | st.wlo);
+      const uint64_t wj = seg_or<W>(w);
+      st.hash = (st.hash ^ wj) * kHashMul;
+      st.served += (uint64_t)__popcll(wj);
+      st.wlo = 0;
     }
   }
 }
 
-// Jobs of workgroup b: wavefront v holds jobs b*64*JPL*kWaves/W + v*JW*JPL +
-// j*JW + lane/W for job sets j < JPL, JW = 64/W.
-template <int W, int JPL, int SMAX, bool USIG>
+// LDS bytes of the shared-trace kernel: model records of the four
+// wavefronts, the stage-latency table [M][Cp][SMAX] (Cp = C rounded up to a
+// power of two) and the trace chunk.
+__host__ __device__ constexpr size_t shared_lds_bytes(int M, int Cp, int SMAX) {
+  return (size_t)kWaves * M * ((size_t)1 << (SMAX <= 4 ? 6 : 7)) + (size_t)M * Cp * SMAX * 8 +
+         (size_t)kChunk * 12;
+}
+
+// Jobs of workgroup b: wavefront v holds jobs b*kWaves*JW + v*JW + lane/W,
+// JW = 64/W.
+template <int W, int SMAX, bool USIG>
 __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   constexpr int JW = 64 / W;
-  constexpr int kSlots = JW * JPL * kWaves;
+  constexpr int kSlots = JW * kWaves;
+  constexpr int RSH = rec_shift<SMAX>();
   extern __shared__ __align__(16) unsigned char smem[];
   int cp = 1, lshift = 0;
   while (cp < a.C) cp <<= 1;
   while ((1 << lshift) < cp * SMAX * 8) ++lshift;
-  double* sL = reinterpret_cast<double*>(smem);  // [M][Cp][SMAX]
-  double* sS = sL + (size_t)a.M * cp * SMAX;     // [M] SLO (one scale) or d_single
-  double* sT = sS + a.M;                         // chunk times
+  unsigned char* sR = smem;                                                        // records
+  double* sL = reinterpret_cast<double*>(sR + (size_t)kWaves * a.M * (1 << RSH));  // [M][Cp][SMAX]
+  double* sT = sL + (size_t)a.M * cp * SMAX;                                       // chunk times
   int32_t* sM = reinterpret_cast<int32_t*>(sT + kChunk);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int seg_lane = lane & (W - 1);
-  const int64_t job0 = (int64_t)blockIdx.x * kSlots + wave * JW * JPL + lane / W;
+  const int64_t job = (int64_t)blockIdx.x * kSlots + wave * JW + lane / W;
+  const bool job_ok = job < a.J;
 
-  SharedConst<JPL> c;
-  bool job_ok[JPL];
-  int cfg_j[JPL];
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) {
-    const int64_t job = job0 + j * JW;
-    job_ok[j] = job < a.J;
-    int p = 0;
-    c.sigma[j] = 0.0;
-    if (job_ok[j]) {
-      p = (int)(job / a.K);
-      c.sigma[j] = a.slo_scale[job % a.K];
-    }
-    int cfg = -1;
-    if (job_ok[j] && seg_lane < a.G) cfg = a.group_cfg[(int64_t)p * a.G + seg_lane];
-    if (cfg >= a.C || cfg < 0) cfg = -1;
-    cfg_j[j] = cfg;
-    uint64_t hb = 0;
-    if (cfg >= 0) {
-      const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
-      for (int m = 0; m < a.M; ++m) hb |= ((hm[m] >> seg_lane) & 1u) << m;
-    }
-    c.hostbits[j] = hb;
-    c.frow[j] = -1;
-    if (job_ok[j])
-      for (int f = 0; f < a.n_finish; ++f)
-        if (a.finish_jobs[f] == job) {
-          c.frow[j] = f;
-          break;
-        }
+  SharedConst c;
+  int p = 0;
+  c.sigma = 0.0;
+  if (job_ok) {
+    p = (int)(job / a.K);
+    c.sigma = a.slo_scale[job % a.K];
   }
-  // single[m]: every job of the wavefront has at most one group hosting m
-  {
-    uint64_t single = 0;
-    for (int m = 0; m < a.M; ++m) {
-      bool ok = true;
-#pragma unroll
-      for (int j = 0; j < JPL; ++j) {
-        const uint64_t hm = __builtin_amdgcn_ballot_w64((c.hostbits[j] >> m) & 1u);
-        ok = ok && lowest_per_field<W>(hm) == hm;
+  int cfg = -1;
+  if (job_ok && seg_lane < a.G) cfg = a.group_cfg[(int64_t)p * a.G + seg_lane];
+  if (cfg >= a.C || cfg < 0) cfg = -1;
+  uint64_t hostbits = 0;  // bit m: this lane's group hosts model m
+  if (cfg >= 0) {
+    const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
+    for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> seg_lane) & 1u) << m;
+  }
+  c.frow = -1;
+  if (job_ok)
+    for (int f = 0; f < a.n_finish; ++f)
+      if (a.finish_jobs[f] == job) {
+        c.frow = f;
+        break;
       }
-      if (ok) single |= 1ull << m;
-    }
-    c.single = single;
-  }
+  const bool wave_finish = __builtin_amdgcn_ballot_w64(c.frow >= 0) != 0;
+  // one configuration for every group of the wavefront?
+  const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
+  const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
+  const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
   const int seg_start = lane & ~(W - 1);
   c.segmask = (W == 64 ? ~0ull : ((1ull << W) - 1)) << seg_start;
-  // do the job sets of every lane of the wavefront share one configuration?
-  bool same = true;
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) {
-    c.lrow[j] = sL + (cfg_j[j] < 0 ? 0 : cfg_j[j]) * SMAX;
-    same = same && (cfg_j[j] < 0 || cfg_j[0] < 0 || cfg_j[j] == cfg_j[0]);
-  }
-  if (cfg_j[0] < 0)
-#pragma unroll
-    for (int j = 1; j < JPL; ++j)
-      if (cfg_j[j] >= 0) c.lrow[0] = c.lrow[j];
-  const bool lsh = JPL == 1 || __builtin_amdgcn_ballot_w64(!same) == 0;
+  c.lrow = sL + (cfg < 0 ? 0 : cfg) * SMAX;
   c.lshift = lshift;
-  c.slo = sS;
   c.seg_lane = seg_lane;
-  bool any_finish = false;
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) any_finish = any_finish || c.frow[j] >= 0;
-  const bool wave_finish = __builtin_amdgcn_ballot_w64(any_finish) != 0;
+  unsigned char* rec = sR + (size_t)wave * a.M * (1 << RSH);
+  c.rec = rec;
 
   // stage-latency table padded with zero-latency stages (see sim_kernel.hpp)
   const int nL = a.M * cp * SMAX;
@@ -315,18 +316,33 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
                   ? a.stage_lat[((int64_t)m * a.C + cc) * a.smax_in + s]
                   : 0.0;
   }
-  // one scale: the SLO of every model, scale * d_single[m] (one rounding)
-  for (int m = tid; m < a.M; m += kThreads)
-    sS[m] = USIG ? a.slo_scale[0] * a.d_single[m] : a.d_single[m];
-
-  SharedLane<JPL, SMAX> st;
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) {
-#pragma unroll
-    for (int s = 0; s < SMAX; ++s) st.F[j][s] = 0.0;
-    st.fin_sum[j] = st.hash[j] = st.served[j] = 0;
-    st.wlo[j] = 0;
+  // this wavefront's model records
+  for (int m = 0; m < a.M; ++m) {
+    const uint64_t hm = __builtin_amdgcn_ballot_w64((hostbits >> m) & 1u);
+    if (lane == 0) {
+      const uint64_t one = lowest_per_field<W>(hm);  // lowest hosting lane of each job
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecMask) = hm;
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount) =
+          one == hm ? 0u : (uint32_t)__builtin_popcountll(one);
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount + 8) = 0;
+    }
   }
+  for (int m = lane; m < a.M; m += 64) {
+    unsigned char* r = rec + ((size_t)m << RSH);
+    // one scale: the SLO, scale * d_single[m] (one rounding); else d_single[m]
+    *(double*)(r + kRecSlo) = USIG ? a.slo_scale[0] * a.d_single[m] : a.d_single[m];
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s)
+      ((double*)(r + kRecLat))[s] = (uni && s < a.cfg_stages[cfg0])
+                                        ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + s]
+                                        : 0.0;
+  }
+
+  SharedLane<SMAX> st;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
+  st.fin_sum = st.hash = st.served = 0;
+  st.wlo = 0;
 
   const int64_t n = a.n;
   for (int64_t base = 0; base < n; base += kChunk) {
@@ -337,30 +353,26 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
       sM[e] = a.model[base + e];
     }
     __syncthreads();
-    if (lsh) {
+    if (uni) {
       if (wave_finish)
-        fast_chunk<W, JPL, SMAX, USIG, true, true>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, true, true>(st, c, sT, sM, cnt, base, n, a.out_finish);
       else
-        fast_chunk<W, JPL, SMAX, USIG, false, true>(st, c, sT, sM, cnt, base, n, a.out_finish);
-    } else if constexpr (JPL > 1) {
+        fast_chunk<W, SMAX, USIG, false, true>(st, c, sT, sM, cnt, base, n, a.out_finish);
+    } else {
       if (wave_finish)
-        fast_chunk<W, JPL, SMAX, USIG, true, false>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, true, false>(st, c, sT, sM, cnt, base, n, a.out_finish);
       else
-        fast_chunk<W, JPL, SMAX, USIG, false, false>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, false, false>(st, c, sT, sM, cnt, base, n, a.out_finish);
     }
   }
 
-#pragma unroll
-  for (int j = 0; j < JPL; ++j) {
-    const int64_t job = job0 + j * JW;
-    const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum[j]);
-    if (job_ok[j] && seg_lane == 0) {
-      a.out_served[job] = (int64_t)st.served[j];
-      if (a.out_attain) a.out_attain[job] = n > 0 ? (double)st.served[j] / (double)n : 0.0;
-      if (a.out_digest) {
-        a.out_digest[2 * job] = st.hash[j];
-        a.out_digest[2 * job + 1] = fin_sum;
-      }
+  const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum);
+  if (job_ok && seg_lane == 0) {
+    a.out_served[job] = (int64_t)st.served;
+    if (a.out_attain) a.out_attain[job] = n > 0 ? (double)st.served / (double)n : 0.0;
+    if (a.out_digest) {
+      a.out_digest[2 * job] = st.hash;
+      a.out_digest[2 * job + 1] = fin_sum;
     }
   }
 }

@@ -134,3 +134,25 @@ def test_sweep_subset_matches_oracle(dev):
     res = api.sweep_results(ds)
     fins = set(int(x) for x in sp.finish_jobs)
     _compare_sweep(sp, res, _oracle_sweep(sp, range(len(pts)), fins))
+
+
+def test_sweep_full_size_sampled(dev):
+    """The whole 4096-point sweep (about 4.4e8 requests in 4096 segments) in the
+    benchmark's launch configuration: the oracle recomputes a sample of jobs,
+    two diagonal per-request output rows among them; every job's counts obey
+    0 <= served <= segment length and attain = served / length exactly."""
+    from paper_2302_11665_amd import api
+    from paper_2302_11665_amd.workload import problems
+    gcfg, hm = _c5_placement()
+    sp = problems.c5_sweep(gcfg, hm)
+    say("sweep full", len(sp.job_segment), "jobs", len(sp.t), "requests")
+    ds = api.upload_sweep(sp)
+    api.run_sweep(ds)
+    res = api.sweep_results(ds)
+    lens = np.diff(sp.seg_offsets)[sp.job_segment]
+    assert np.all(res["served"] >= 0) and np.all(res["served"] <= lens)
+    assert np.array_equal(res["attain"], np.where(lens > 0, res["served"] / np.maximum(lens, 1), 0.0))
+    rng = np.random.default_rng(55)
+    fins = {int(sp.finish_jobs[0]), int(sp.finish_jobs[-1])}
+    jobs = sorted(set(rng.choice(len(sp.job_segment), 10, replace=False).tolist()) | fins)
+    _compare_sweep(sp, res, _oracle_sweep(sp, jobs, fins))

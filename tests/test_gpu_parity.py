@@ -16,11 +16,10 @@ pytestmark = pytest.mark.gpu
 
 
 # kernel selections the library offers (environment variables read per call):
-# the shared-trace kernel with one or two jobs per lane, and the general
-# LDS-staged kernel with one or two groups per lane
+# the shared-trace kernel (one group per lane), and the general LDS-staged
+# kernel with one or two groups per lane
 VARIANTS = {
     "shared": {},
-    "shared_jpl2": {"ALPASERVE_JPL": "2"},
     "lds": {"ALPASERVE_PATH": "lds", "ALPASERVE_GPL": "1"},
     "lds_gpl2": {"ALPASERVE_PATH": "lds", "ALPASERVE_GPL": "2"},
 }
@@ -38,7 +37,7 @@ def gpu_api():
 
 @pytest.fixture(params=sorted(VARIANTS))
 def gpu(request, gpu_api, monkeypatch):
-    for k in ("ALPASERVE_JPL", "ALPASERVE_PATH", "ALPASERVE_GPL"):
+    for k in ("ALPASERVE_PATH", "ALPASERVE_GPL"):
         monkeypatch.delenv(k, raising=False)
     for k, v in VARIANTS[request.param].items():
         monkeypatch.setenv(k, v)
