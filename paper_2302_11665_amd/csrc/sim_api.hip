@@ -2,6 +2,7 @@
 // launches on the caller's stream, error reporting.  See alpaserve_sim.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -283,6 +284,13 @@ __global__ void validate_kernel(const double* t, const int32_t* model, int64_t n
   if (bad) atomicOr(flags, bad);
 }
 
+// Fill p[0, n) with v (per-request output rows before a shared-trace launch).
+__global__ void fill_f64(double* __restrict__ p, int64_t n, double v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
 // Launch the batched simulation of a shared trace (a fully filled except the
 // kernel shape).  W is the group count on entry.
 int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
@@ -293,7 +301,17 @@ int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
   const size_t lds_shared = as_dev::shared_lds_bytes(a.M, pow2ceil(a.C), smax);
   if (use_shared_path() && lds_shared <= shared_lds_limit()) {
     const int Ws = pow2ceil(a.G);
-    hipError_t e = launch_shared_any(Ws, smax, a.K == 1, a, lds_shared, stream);
+    hipError_t e = hipSuccess;
+    if (a.n_finish > 0 && a.n > 0) {
+      // rows start at -2 (no hosting group); the kernel writes the others
+      const int64_t cells = (int64_t)a.n_finish * a.n;
+      const int64_t blocks = std::min<int64_t>((cells + 255) / 256, 8192);
+      hipLaunchKernelGGL(fill_f64, dim3((unsigned)blocks), dim3(256), 0, stream, a.out_finish,
+                         cells, -2.0);
+      if ((e = hipGetLastError()) != hipSuccess)
+        return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    }
+    e = launch_shared_any(Ws, smax, a.K == 1, a, lds_shared, stream);
     if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
   }

@@ -108,9 +108,9 @@ struct SharedConst {
   const double* lrow;        // stage-latency row of this lane's configuration for model 0 (LDS)
   int lshift;                // log2 of the per-model row stride (bytes) of that table
   double sigma;              // this job's scale (used when jobs differ in scale)
-  uint64_t segmask;          // lanes of this lane's job
-  int seg_lane;
-  int frow;                  // per-request output row of this job, -1 if none
+  uint64_t fmask;            // lanes of the wavefront's jobs with per-request output
+  double* frowp;             // this job's per-request output row (lanes in fmask),
+                             // filled with -2 before the launch
 };
 
 // One request at trace position i.  hm: the wavefront's hosting lanes; cnt:
@@ -155,11 +155,9 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
   st.fin_sum += acc ? (uint64_t)__double_as_longlong(f) : 0ull;
   sr = (sr << 1) | (acc ? 1u : 0u);
   if constexpr (FINISH) {
-    if (c.frow >= 0) {
-      double* dst = out_finish + (int64_t)c.frow * n + i;
-      if (__builtin_amdgcn_inverse_ballot_w64(cm)) *dst = acc ? f : -1.0;
-      else if ((cm & c.segmask) == 0 && c.seg_lane == 0) *dst = -2.0;
-    }
+    // per-request output: the job's target lane writes the finish time, or
+    // -1 if rejected; rows start filled with -2 (a request no group hosts)
+    if (__builtin_amdgcn_inverse_ballot_w64(cm & c.fmask)) c.frowp[i] = acc ? f : -1.0;
   }
 }
 
@@ -248,7 +246,7 @@ __host__ __device__ constexpr size_t shared_lds_bytes(int M, int Cp, int SMAX) {
 }
 
 // Jobs of workgroup b: wavefront v holds jobs b*kWaves*JW + v*JW + lane/W,
-// JW = 64/W.
+// JW = 64/W.  Per-request output rows must hold -2 when the kernel starts.
 template <int W, int SMAX, bool USIG>
 __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   constexpr int JW = 64 / W;
@@ -285,23 +283,22 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
     const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
     for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> seg_lane) & 1u) << m;
   }
-  c.frow = -1;
+  int frow = -1;  // per-request output row of this job, -1 if none
   if (job_ok)
     for (int f = 0; f < a.n_finish; ++f)
       if (a.finish_jobs[f] == job) {
-        c.frow = f;
+        frow = f;
         break;
       }
-  const bool wave_finish = __builtin_amdgcn_ballot_w64(c.frow >= 0) != 0;
+  c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
+  c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.n);
+  const bool wave_finish = c.fmask != 0;
   // one configuration for every group of the wavefront?
   const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
   const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
   const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
-  const int seg_start = lane & ~(W - 1);
-  c.segmask = (W == 64 ? ~0ull : ((1ull << W) - 1)) << seg_start;
   c.lrow = sL + (cfg < 0 ? 0 : cfg) * SMAX;
   c.lshift = lshift;
-  c.seg_lane = seg_lane;
   unsigned char* rec = sR + (size_t)wave * a.M * (1 << RSH);
   c.rec = rec;
 
