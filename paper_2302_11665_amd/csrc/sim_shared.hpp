@@ -6,6 +6,9 @@
 // wavefronts per workgroup.  The trace is staged through LDS in chunks read
 // with coalesced loads by the whole workgroup (each request is read from
 // HBM/L2 once per workgroup); every wavefront then reads the same words.
+// Staging also stores each request's model-record offset and, when one SLO
+// scale serves every job, its deadline t + SLO (computed once per workgroup
+// instead of once per wavefront).
 //
 // Per-wavefront model records (LDS, one per model m, built when the kernel
 // starts): the wavefront's hosting lane mask for m (bit l = lane l's group
@@ -87,13 +90,12 @@ __device__ __forceinline__ uint32_t seg_min_u32(uint32_t x) {
   return x;
 }
 
-// Bytes of one model record: hosting mask (8), SLO or d_single (8), count
-// (4), padding (12), stage latencies (8 * SMAX); a power of two.
-template <int SMAX>
-constexpr int rec_shift() {
-  return SMAX <= 4 ? 6 : 7;
-}
-constexpr int kRecMask = 0, kRecSlo = 8, kRecCount = 16, kRecLat = 32;
+// Layout of one model record: hosting mask (u64) at 0, count (u32) at 8,
+// stage latencies (SMAX doubles) at 16, SLO or d_single (double) after them;
+// the record size is a power of two.
+constexpr int kRecMask = 0, kRecCount = 8, kRecLat = 16;
+__host__ __device__ constexpr int rec_slo(int SMAX) { return kRecLat + 8 * SMAX; }
+__host__ __device__ constexpr int rec_shift(int SMAX) { return SMAX == 1 ? 5 : (SMAX <= 4 ? 6 : 7); }
 
 // Per-lane state: group (lane mod W) of one job.
 template <int SMAX>
@@ -113,13 +115,27 @@ struct SharedConst {
                              // filled with -2 before the launch
 };
 
+// Projection through this lane's stage chain (Sec. 3.4): fs[s] is the
+// request's finish time at stage s; returns the last.
+template <int SMAX>
+__device__ __forceinline__ double chain(const SharedLane<SMAX>& st, double ti,
+                                        const double (&L)[SMAX], double (&fs)[SMAX]) {
+  double f = ti;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    fs[s] = vmax(f, st.F[s]) + L[s];
+    f = fs[s];
+  }
+  return f;
+}
+
 // One request at trace position i.  hm: the wavefront's hosting lanes; cnt:
-// the record's count; L: this lane's stage latencies of the model; sv: the
-// SLO (USIG) or d_single of the model.
+// the record's count; L: this lane's stage latencies of the model; dv: the
+// deadline t + SLO (USIG, staged with the trace) or d_single of the model.
 template <int W, int SMAX, bool USIG, bool FINISH>
 __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedConst& c, double ti,
                                           uint64_t hm, uint32_t cnt, const double (&L)[SMAX],
-                                          double sv, int64_t i, int64_t n,
+                                          double dv, int64_t i, int64_t n,
                                           double* __restrict__ out_finish, uint32_t& sr) {
   uint64_t cm = hm;  // the dispatch target of every job: one lane per job or none
   if (cnt != 0) {
@@ -138,16 +154,10 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
       cm = lowest_per_field<W>(__builtin_amdgcn_ballot_w64(klo == mlo) & eqhi);
     }
   }
-  // projection through this lane's stage chain (Sec. 3.4)
   double fs[SMAX];
-  double f = ti;
-#pragma unroll
-  for (int s = 0; s < SMAX; ++s) {
-    fs[s] = vmax(f, st.F[s]) + L[s];
-    f = fs[s];
-  }
+  const double f = chain<SMAX>(st, ti, L, fs);
   // admission (Sec. 4.3, Sec. 3.2) and commit on the target lane
-  const double deadline = ti + (USIG ? sv : c.sigma * sv);
+  const double deadline = USIG ? dv : ti + c.sigma * dv;
   const uint64_t am = cm & __builtin_amdgcn_ballot_w64(!(f > deadline));
   const bool acc = __builtin_amdgcn_inverse_ballot_w64(am);
 #pragma unroll
@@ -161,34 +171,47 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
   }
 }
 
-// Requests [i0, i0 + B) from the LDS chunk: read all of their inputs first
-// (LDS reads in flight together), then run them in order.  UNI: every group
-// of the wavefront has the same configuration, whose stage latencies the
-// model records hold; otherwise each lane reads its configuration's row.
+// Requests [i0, i0 + B) from the LDS chunk (cTD: {t, deadline} pairs, cO:
+// record offsets): read all of their inputs first (LDS reads in flight
+// together), then run them in order.  UNI: every group of the wavefront has
+// the same configuration, whose stage latencies the model records hold;
+// otherwise each lane reads its configuration's row.
 template <int W, int SMAX, int B, bool USIG, bool FINISH, bool UNI>
 __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedConst& c,
-                                           const double* __restrict__ cT,
-                                           const int32_t* __restrict__ cM, int64_t i0, int64_t n,
+                                           const double* __restrict__ cTD,
+                                           const uint32_t* __restrict__ cO, int64_t i0, int64_t n,
                                            double* __restrict__ out_finish, uint32_t& sr) {
-  double t[B], sv[B], L[B][SMAX];
+  double t[B], dv[B], L[B][SMAX];
   uint64_t hmv[B];
-  uint32_t cnv[B];
-  int m[B];
+  uint32_t cnv[B], off[B];
 #pragma unroll
   for (int k = 0; k < B; ++k) {
-    t[k] = cT[k];
-    m[k] = cM[k];
+    t[k] = cTD[2 * k];
+    if (USIG) dv[k] = cTD[2 * k + 1];
+    off[k] = cO[k];
   }
 #pragma unroll
   for (int k = 0; k < B; ++k) {
-    const unsigned char* r = c.rec + ((unsigned)m[k] << rec_shift<SMAX>());
-    hmv[k] = *(const uint64_t*)(r + kRecMask);
-    sv[k] = *(const double*)(r + kRecSlo);
-    cnv[k] = *(const uint32_t*)(r + kRecCount);
-    const double* lr = UNI ? (const double*)(r + kRecLat)
-                           : (const double*)((const char*)c.lrow + ((unsigned)m[k] << c.lshift));
+    // records are 32-byte aligned: 16-byte loads
+    const unsigned char* r = c.rec + off[k];
+    const uint4 head = *(const uint4*)(r + kRecMask);  // hosting mask, count
+    hmv[k] = ((uint64_t)head.y << 32) | head.x;
+    cnv[k] = head.z;
+    if (!USIG) dv[k] = *(const double*)(r + rec_slo(SMAX));
+    if (UNI) {
 #pragma unroll
-    for (int s = 0; s < SMAX; ++s) L[k][s] = lr[s];
+      for (int s = 0; s + 1 < SMAX; s += 2) {
+        const double2 l2 = *(const double2*)(r + kRecLat + 8 * s);
+        L[k][s] = l2.x;
+        L[k][s + 1] = l2.y;
+      }
+      if (SMAX & 1) L[k][SMAX - 1] = *(const double*)(r + kRecLat + 8 * (SMAX - 1));
+    } else {
+      const double* lr =
+          (const double*)((const char*)c.lrow + ((off[k] >> rec_shift(SMAX)) << c.lshift));
+#pragma unroll
+      for (int s = 0; s < SMAX; ++s) L[k][s] = lr[s];
+    }
   }
 #pragma unroll
   for (int k = 0; k < B; ++k) {
@@ -196,7 +219,7 @@ __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedCon
     const uint64_t hm = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(hmv[k] >> 32)) << 32) |
                         (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)hmv[k]);
     const uint32_t cnt = (uint32_t)__builtin_amdgcn_readfirstlane((int)cnv[k]);
-    fast_step<W, SMAX, USIG, FINISH>(st, c, t[k], hm, cnt, L[k], sv[k], i0 + k, n, out_finish, sr);
+    fast_step<W, SMAX, USIG, FINISH>(st, c, t[k], hm, cnt, L[k], dv[k], i0 + k, n, out_finish, sr);
   }
 }
 
@@ -204,8 +227,8 @@ __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedCon
 // 64-request accept words.
 template <int W, int SMAX, bool USIG, bool FINISH, bool UNI>
 __device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedConst& c,
-                                           const double* __restrict__ cT,
-                                           const int32_t* __restrict__ cM, int cnt, int64_t base,
+                                           const double* __restrict__ cTD,
+                                           const uint32_t* __restrict__ cO, int cnt, int64_t base,
                                            int64_t n, double* __restrict__ out_finish) {
   constexpr int B = SMAX <= 4 ? 4 : 2;
   for (int h = 0; h < cnt; h += 32) {
@@ -213,12 +236,12 @@ __device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedCon
     uint32_t sr = 0;
     if (hc == 32) {
       for (int e = 0; e < 32; e += B)
-        fast_batch<W, SMAX, B, USIG, FINISH, UNI>(st, c, cT + h + e, cM + h + e, base + h + e, n,
-                                                  out_finish, sr);
+        fast_batch<W, SMAX, B, USIG, FINISH, UNI>(st, c, cTD + 2 * (h + e), cO + h + e,
+                                                  base + h + e, n, out_finish, sr);
     } else {
       for (int e = 0; e < hc; ++e)
-        fast_batch<W, SMAX, 1, USIG, FINISH, UNI>(st, c, cT + h + e, cM + h + e, base + h + e, n,
-                                                  out_finish, sr);
+        fast_batch<W, SMAX, 1, USIG, FINISH, UNI>(st, c, cTD + 2 * (h + e), cO + h + e,
+                                                  base + h + e, n, out_finish, sr);
     }
     const int64_t pos = (base + h) & 63;  // 0 or 32
     const bool end = base + h + hc == n;
@@ -239,10 +262,10 @@ __device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedCon
 
 // LDS bytes of the shared-trace kernel: model records of the four
 // wavefronts, the stage-latency table [M][Cp][SMAX] (Cp = C rounded up to a
-// power of two) and the trace chunk.
+// power of two) and the trace chunk ({t, deadline} pairs and record offsets).
 __host__ __device__ constexpr size_t shared_lds_bytes(int M, int Cp, int SMAX) {
-  return (size_t)kWaves * M * ((size_t)1 << (SMAX <= 4 ? 6 : 7)) + (size_t)M * Cp * SMAX * 8 +
-         (size_t)kChunk * 12;
+  return (size_t)kWaves * M * ((size_t)1 << rec_shift(SMAX)) + (size_t)M * Cp * SMAX * 8 +
+         (size_t)kChunk * 20;
 }
 
 // Jobs of workgroup b: wavefront v holds jobs b*kWaves*JW + v*JW + lane/W,
@@ -251,15 +274,15 @@ template <int W, int SMAX, bool USIG>
 __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   constexpr int JW = 64 / W;
   constexpr int kSlots = JW * kWaves;
-  constexpr int RSH = rec_shift<SMAX>();
+  constexpr int RSH = rec_shift(SMAX);
   extern __shared__ __align__(16) unsigned char smem[];
   int cp = 1, lshift = 0;
   while (cp < a.C) cp <<= 1;
   while ((1 << lshift) < cp * SMAX * 8) ++lshift;
   unsigned char* sR = smem;                                                        // records
   double* sL = reinterpret_cast<double*>(sR + (size_t)kWaves * a.M * (1 << RSH));  // [M][Cp][SMAX]
-  double* sT = sL + (size_t)a.M * cp * SMAX;                                       // chunk times
-  int32_t* sM = reinterpret_cast<int32_t*>(sT + kChunk);
+  double* sTD = sL + (size_t)a.M * cp * SMAX;                      // chunk {t, deadline}
+  uint32_t* sO = reinterpret_cast<uint32_t*>(sTD + 2 * kChunk);    // chunk record offsets
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -293,6 +316,9 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
   c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.n);
   const bool wave_finish = c.fmask != 0;
+  // a wavefront with per-request output has more to issue per request than
+  // the others and sets the launch time: let it issue first on its SIMD
+  if (wave_finish) __builtin_amdgcn_s_setprio(3);
   // one configuration for every group of the wavefront?
   const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
   const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
@@ -321,13 +347,12 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
       *(uint64_t*)(rec + ((size_t)m << RSH) + kRecMask) = hm;
       *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount) =
           one == hm ? 0u : (uint32_t)__builtin_popcountll(one);
-      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount + 8) = 0;
     }
   }
   for (int m = lane; m < a.M; m += 64) {
     unsigned char* r = rec + ((size_t)m << RSH);
     // one scale: the SLO, scale * d_single[m] (one rounding); else d_single[m]
-    *(double*)(r + kRecSlo) = USIG ? a.slo_scale[0] * a.d_single[m] : a.d_single[m];
+    *(double*)(r + rec_slo(SMAX)) = USIG ? a.slo_scale[0] * a.d_single[m] : a.d_single[m];
 #pragma unroll
     for (int s = 0; s < SMAX; ++s)
       ((double*)(r + kRecLat))[s] = (uni && s < a.cfg_stages[cfg0])
@@ -346,20 +371,25 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
     const int cnt = (int)((n - base) < kChunk ? (n - base) : kChunk);
     __syncthreads();
     for (int e = tid; e < cnt; e += kThreads) {
-      sT[e] = a.t[base + e];
-      sM[e] = a.model[base + e];
+      const double te = a.t[base + e];
+      const uint32_t off = (uint32_t)a.model[base + e] << RSH;
+      // one scale: the deadline t + SLO (one rounding) is the same for every
+      // job; the SLO is read from wave 0's record (all waves hold it)
+      const double de = USIG ? te + *(const double*)(sR + off + rec_slo(SMAX)) : te;
+      *(double2*)(sTD + 2 * e) = make_double2(te, de);
+      sO[e] = off;
     }
     __syncthreads();
     if (uni) {
       if (wave_finish)
-        fast_chunk<W, SMAX, USIG, true, true>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, true, true>(st, c, sTD, sO, cnt, base, n, a.out_finish);
       else
-        fast_chunk<W, SMAX, USIG, false, true>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, false, true>(st, c, sTD, sO, cnt, base, n, a.out_finish);
     } else {
       if (wave_finish)
-        fast_chunk<W, SMAX, USIG, true, false>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, true, false>(st, c, sTD, sO, cnt, base, n, a.out_finish);
       else
-        fast_chunk<W, SMAX, USIG, false, false>(st, c, sT, sM, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, false, false>(st, c, sTD, sO, cnt, base, n, a.out_finish);
     }
   }
 
