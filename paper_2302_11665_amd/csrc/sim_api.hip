@@ -291,6 +291,22 @@ __global__ void fill_f64(double* __restrict__ p, int64_t n, double v) {
     p[i] = v;
 }
 
+// Fill the per-request output rows of segmented jobs with -2 over
+// [0, min(segment length, finish_stride)) (the rest stays untouched).
+__global__ void fill_seg_rows(const KArgs a) {
+  const int64_t total = (int64_t)a.n_finish * a.finish_stride;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int f = (int)(i / a.finish_stride);
+    const int64_t k = i % a.finish_stride;
+    int p = 0;
+    double sigma = 0.0;
+    int64_t begin = 0, len = 0;
+    as_dev::seg_job(a, a.finish_jobs[f], p, sigma, begin, len);
+    if (k < len) a.out_finish[i] = -2.0;
+  }
+}
+
 // Launch the batched simulation of a shared trace (a fully filled except the
 // kernel shape).  W is the group count on entry.
 int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
@@ -564,12 +580,29 @@ int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_o
   a.out_attain = out_attain;
   a.out_digest = out_digest;
   a.finish_stride = finish_stride;
+  hipStream_t s = (hipStream_t)stream;
+  // more than 32 groups: one job per wavefront with the shared-trace request
+  // loop (the requests of a wavefront are one job's)
+  const size_t lds_seg = as_dev::seg_lds_bytes(a.M, pow2ceil(a.C), smax);
+  if (use_shared_path() && pow2ceil(a.G) == 64 && lds_seg <= shared_lds_limit()) {
+    hipError_t e = hipSuccess;
+    if (a.n_finish > 0 && finish_stride > 0) {
+      const int64_t cells = (int64_t)a.n_finish * finish_stride;
+      const int64_t blocks = std::min<int64_t>((cells + 255) / 256, 8192);
+      hipLaunchKernelGGL(fill_seg_rows, dim3((unsigned)blocks), dim3(256), 0, s, a);
+      if ((e = hipGetLastError()) != hipSuccess)
+        return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    }
+    e = as_host::launch_seg64(smax, a, lds_seg, s);
+    if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return ok();
+  }
   int GPL = 1;
   if (!choose_shape(a.G, n_jobs, true, a.M, a.C, smax, W, GPL))
     return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
                 a.M, a.C, smax);
   const size_t lds = lds_bytes(W, smax, true, a.M, a.C);
-  hipError_t e = launch_lds_any(W, GPL, smax, true, a, lds, (hipStream_t)stream);
+  hipError_t e = launch_lds_any(W, GPL, smax, true, a, lds, s);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -69,6 +69,27 @@ hipError_t launch_shared(int smax, bool usig, const KArgs& a, size_t lds, hipStr
   }
 }
 
+#if AS_W == 64
+hipError_t launch_seg64(int smax, const KArgs& a, size_t lds, hipStream_t s) {
+  const int grid = (a.J + as_dev::kWaves - 1) / as_dev::kWaves;
+  switch (smax) {
+    case 1:
+      hipLaunchKernelGGL((as_dev::seg_kernel<1>), dim3(grid), dim3(as_dev::kThreads), lds, s, a);
+      break;
+    case 2:
+      hipLaunchKernelGGL((as_dev::seg_kernel<2>), dim3(grid), dim3(as_dev::kThreads), lds, s, a);
+      break;
+    case 4:
+      hipLaunchKernelGGL((as_dev::seg_kernel<4>), dim3(grid), dim3(as_dev::kThreads), lds, s, a);
+      break;
+    default:
+      hipLaunchKernelGGL((as_dev::seg_kernel<8>), dim3(grid), dim3(as_dev::kThreads), lds, s, a);
+      break;
+  }
+  return hipGetLastError();
+}
+#endif
+
 template hipError_t launch_lds<AS_W>(int, int, bool, const KArgs&, size_t, hipStream_t);
 template hipError_t launch_shared<AS_W>(int, bool, const KArgs&, size_t, hipStream_t);
 

@@ -18,6 +18,10 @@ hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, h
 template <int W>
 hipError_t launch_shared(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s);
 
+// Segmented jobs with up to 64 groups, one job per wavefront (built in the
+// 64-lane unit).
+hipError_t launch_seg64(int smax, const KArgs& a, size_t lds, hipStream_t s);
+
 #define AS_DECLARE_W(W)                                                                       \
   extern template hipError_t launch_lds<W>(int, int, bool, const KArgs&, size_t, hipStream_t); \
   extern template hipError_t launch_shared<W>(int, bool, const KArgs&, size_t, hipStream_t);

@@ -70,22 +70,27 @@ __device__ __forceinline__ uint64_t lowest_per_field(uint64_t b) {
 __device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
 // Unsigned minimum over each aligned W-lane segment, in every lane of it.
-// Inside a 16-lane row each step is one v_min_u32 with a DPP operand; the
-// 16- and 32-lane steps swap rows / halves with v_permlane16/32_swap (both
-// outputs of the swap are the two halves of the butterfly).
+// Inside a 16-lane row each step is one v_min_u32 with a DPP operand; for
+// W = 32 the 16-lane step swaps rows with v_permlane16_swap (its two outputs
+// are the two halves of the butterfly); for W = 64 row broadcasts gather the
+// minimum in lane 63, whose value is returned to every lane.
 template <int W>
 __device__ __forceinline__ uint32_t seg_min_u32(uint32_t x) {
   if constexpr (W >= 2) x = umin32(x, dpp_u32<kXor1>(x));
   if constexpr (W >= 4) x = umin32(x, dpp_u32<kXor2>(x));
   if constexpr (W >= 8) x = umin32(x, dpp_u32<kHalfMirror>(x));
   if constexpr (W >= 16) x = umin32(x, dpp_u32<kMirror>(x));
-  if constexpr (W >= 32) {
+  if constexpr (W == 32) {
     const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
     x = umin32(r[0], r[1]);
   }
-  if constexpr (W >= 64) {
-    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-    x = umin32(r[0], r[1]);
+  if constexpr (W == 64) {
+    // fold the four row minima into lane 63 (row_bcast:15 into rows 1 and 3,
+    // row_bcast:31 into rows 2 and 3; masked-off rows keep their value) and
+    // read it back as a wave-uniform scalar
+    x = umin32(x, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)x, 0x142, 0xa, 0xf, false));
+    x = umin32(x, (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)x, 0x143, 0xc, 0xf, false));
+    x = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
   }
   return x;
 }
@@ -112,7 +117,10 @@ struct SharedConst {
   double sigma;              // this job's scale (used when jobs differ in scale)
   uint64_t fmask;            // lanes of the wavefront's jobs with per-request output
   double* frowp;             // this job's per-request output row (lanes in fmask),
-                             // filled with -2 before the launch
+                             // filled with -2 before the launch; within a chunk:
+                             // the element of the chunk's first request
+  int64_t flimit;            // requests i < flimit have an output element
+  int fcnt;                  // within a chunk: its first fcnt requests have one
 };
 
 // Projection through this lane's stage chain (Sec. 3.4): fs[s] is the
@@ -129,14 +137,13 @@ __device__ __forceinline__ double chain(const SharedLane<SMAX>& st, double ti,
   return f;
 }
 
-// One request at trace position i.  hm: the wavefront's hosting lanes; cnt:
+// One request, number ik of its chunk.  hm: the wavefront's hosting lanes; cnt:
 // the record's count; L: this lane's stage latencies of the model; dv: the
 // deadline t + SLO (USIG, staged with the trace) or d_single of the model.
-template <int W, int SMAX, bool USIG, bool FINISH>
+template <int W, int SMAX, bool USIG, bool FINISH, bool FLIM>
 __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedConst& c, double ti,
                                           uint64_t hm, uint32_t cnt, const double (&L)[SMAX],
-                                          double dv, int64_t i, int64_t n,
-                                          double* __restrict__ out_finish, uint32_t& sr) {
+                                          double dv, int ik, uint32_t& sr) {
   uint64_t cm = hm;  // the dispatch target of every job: one lane per job or none
   if (cnt != 0) {
     const bool hosted = __builtin_amdgcn_inverse_ballot_w64(hm);
@@ -167,20 +174,20 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
   if constexpr (FINISH) {
     // per-request output: the job's target lane writes the finish time, or
     // -1 if rejected; rows start filled with -2 (a request no group hosts)
-    if (__builtin_amdgcn_inverse_ballot_w64(cm & c.fmask)) c.frowp[i] = acc ? f : -1.0;
+    if ((!FLIM || ik < c.fcnt) && __builtin_amdgcn_inverse_ballot_w64(cm & c.fmask))
+      c.frowp[ik] = acc ? f : -1.0;
   }
 }
 
-// Requests [i0, i0 + B) from the LDS chunk (cTD: {t, deadline} pairs, cO:
+// Requests [i0, i0 + B) of the LDS chunk (cTD: {t, deadline} pairs, cO:
 // record offsets): read all of their inputs first (LDS reads in flight
 // together), then run them in order.  UNI: every group of the wavefront has
 // the same configuration, whose stage latencies the model records hold;
 // otherwise each lane reads its configuration's row.
-template <int W, int SMAX, int B, bool USIG, bool FINISH, bool UNI>
+template <int W, int SMAX, int B, bool USIG, bool FINISH, bool FLIM, bool UNI>
 __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedConst& c,
                                            const double* __restrict__ cTD,
-                                           const uint32_t* __restrict__ cO, int64_t i0, int64_t n,
-                                           double* __restrict__ out_finish, uint32_t& sr) {
+                                           const uint32_t* __restrict__ cO, int i0, uint32_t& sr) {
   double t[B], dv[B], L[B][SMAX];
   uint64_t hmv[B];
   uint32_t cnv[B], off[B];
@@ -219,29 +226,37 @@ __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedCon
     const uint64_t hm = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(hmv[k] >> 32)) << 32) |
                         (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)hmv[k]);
     const uint32_t cnt = (uint32_t)__builtin_amdgcn_readfirstlane((int)cnv[k]);
-    fast_step<W, SMAX, USIG, FINISH>(st, c, t[k], hm, cnt, L[k], dv[k], i0 + k, n, out_finish, sr);
+    fast_step<W, SMAX, USIG, FINISH, FLIM>(st, c, t[k], hm, cnt, L[k], dv[k], i0 + k, sr);
   }
 }
 
 // All requests of one LDS chunk [base, base + cnt): 32-request halves of
 // 64-request accept words.
-template <int W, int SMAX, bool USIG, bool FINISH, bool UNI>
-__device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedConst& c,
+template <int W, int SMAX, bool USIG, bool FINISH, bool FLIM, bool UNI>
+__device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedConst& c0,
                                            const double* __restrict__ cTD,
                                            const uint32_t* __restrict__ cO, int cnt, int64_t base,
-                                           int64_t n, double* __restrict__ out_finish) {
+                                           int64_t n) {
   constexpr int B = SMAX <= 4 ? 4 : 2;
+  // output row relative to this chunk; FLIM: only the first fcnt requests of
+  // the chunk have an output element (the same for the whole wavefront)
+  SharedConst c = c0;
+  if (FINISH) {
+    c.frowp = c0.frowp + base;
+    if (FLIM) {
+      const int64_t left = c0.flimit - base;
+      c.fcnt = __builtin_amdgcn_readfirstlane(left <= 0 ? 0 : (left < cnt ? (int)left : cnt));
+    }
+  }
   for (int h = 0; h < cnt; h += 32) {
     const int hc = (cnt - h) < 32 ? (cnt - h) : 32;
     uint32_t sr = 0;
     if (hc == 32) {
       for (int e = 0; e < 32; e += B)
-        fast_batch<W, SMAX, B, USIG, FINISH, UNI>(st, c, cTD + 2 * (h + e), cO + h + e,
-                                                  base + h + e, n, out_finish, sr);
+        fast_batch<W, SMAX, B, USIG, FINISH, FLIM, UNI>(st, c, cTD + 2 * (h + e), cO + h + e, h + e, sr);
     } else {
       for (int e = 0; e < hc; ++e)
-        fast_batch<W, SMAX, 1, USIG, FINISH, UNI>(st, c, cTD + 2 * (h + e), cO + h + e,
-                                                  base + h + e, n, out_finish, sr);
+        fast_batch<W, SMAX, 1, USIG, FINISH, FLIM, UNI>(st, c, cTD + 2 * (h + e), cO + h + e, h + e, sr);
     }
     const int64_t pos = (base + h) & 63;  // 0 or 32
     const bool end = base + h + hc == n;
@@ -315,6 +330,7 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
       }
   c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
   c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.n);
+  c.flimit = a.n;
   const bool wave_finish = c.fmask != 0;
   // a wavefront with per-request output has more to issue per request than
   // the others and sets the launch time: let it issue first on its SIMD
@@ -382,14 +398,14 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
     __syncthreads();
     if (uni) {
       if (wave_finish)
-        fast_chunk<W, SMAX, USIG, true, true>(st, c, sTD, sO, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, true, false, true>(st, c, sTD, sO, cnt, base, n);
       else
-        fast_chunk<W, SMAX, USIG, false, true>(st, c, sTD, sO, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, false, false, true>(st, c, sTD, sO, cnt, base, n);
     } else {
       if (wave_finish)
-        fast_chunk<W, SMAX, USIG, true, false>(st, c, sTD, sO, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, true, false, false>(st, c, sTD, sO, cnt, base, n);
       else
-        fast_chunk<W, SMAX, USIG, false, false>(st, c, sTD, sO, cnt, base, n, a.out_finish);
+        fast_chunk<W, SMAX, USIG, false, false, false>(st, c, sTD, sO, cnt, base, n);
     }
   }
 
@@ -397,6 +413,180 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   if (job_ok && seg_lane == 0) {
     a.out_served[job] = (int64_t)st.served;
     if (a.out_attain) a.out_attain[job] = n > 0 ? (double)st.served / (double)n : 0.0;
+    if (a.out_digest) {
+      a.out_digest[2 * job] = st.hash;
+      a.out_digest[2 * job + 1] = fin_sum;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Segmented jobs with up to 64 groups: one job per wavefront (lane g = group
+// g), each job simulating its own trace segment at its own SLO scale.  The
+// requests of a wavefront are again the same in every lane, so the request
+// loop above applies unchanged.  The job's SLOs (scale * d_single[m], one
+// rounding) go into its model records, and each wavefront stages its own
+// segment through its own LDS region -- deadline t + SLO and record offset
+// per request -- with no workgroup barrier in the request loop.
+
+constexpr int kSegChunk = 512;  // requests per staging round of one wavefront
+
+// LDS bytes of seg_kernel: records, the stage-latency table, and each
+// wavefront's chunk ({t, deadline} pairs, record offsets).
+__host__ __device__ constexpr size_t seg_lds_bytes(int M, int Cp, int SMAX) {
+  return (size_t)kWaves * M * ((size_t)1 << rec_shift(SMAX)) + (size_t)M * Cp * SMAX * 8 +
+         (size_t)kWaves * kSegChunk * 20;
+}
+
+// Length and start of job j's segment: a record naming a missing placement or
+// segment makes an empty job; bounds are clamped to [0, seg_off[n_segments]].
+__device__ __forceinline__ void seg_job(const KArgs& a, int64_t j, int& p, double& sigma,
+                                        int64_t& begin, int64_t& len) {
+  const as_job_t jb = a.jobs[j];
+  p = jb.placement;
+  sigma = jb.slo_scale;
+  begin = 0;
+  len = 0;
+  if (p < 0 || p >= a.P || jb.segment < 0 || jb.segment >= a.n_segments) {
+    p = 0;
+    return;
+  }
+  const int64_t total = a.seg_off[a.n_segments];
+  int64_t b = a.seg_off[jb.segment], e = a.seg_off[jb.segment + 1];
+  b = b < 0 ? 0 : (b > total ? total : b);
+  e = e < b ? b : (e > total ? total : e);
+  begin = b;
+  len = e - b;
+}
+
+// Job j = blockIdx.x * kWaves + wavefront.  Per-request output rows must hold
+// -2 over [0, min(segment length, finish_stride)) when the kernel starts.
+template <int SMAX>
+__global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
+  constexpr int W = 64;
+  constexpr int RSH = rec_shift(SMAX);
+  extern __shared__ __align__(16) unsigned char smem[];
+  int cp = 1, lshift = 0;
+  while (cp < a.C) cp <<= 1;
+  while ((1 << lshift) < cp * SMAX * 8) ++lshift;
+  unsigned char* sR = smem;                                                        // records
+  double* sL = reinterpret_cast<double*>(sR + (size_t)kWaves * a.M * (1 << RSH));  // [M][Cp][SMAX]
+  double* sTDall = sL + (size_t)a.M * cp * SMAX;
+  uint32_t* sOall = reinterpret_cast<uint32_t*>(sTDall + (size_t)kWaves * 2 * kSegChunk);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t job = (int64_t)blockIdx.x * kWaves + wave;
+  const bool job_ok = job < a.J;
+  double* sTD = sTDall + (size_t)wave * 2 * kSegChunk;
+  uint32_t* sO = sOall + (size_t)wave * kSegChunk;
+
+  int p = 0;
+  double sigma = 0.0;
+  int64_t begin = 0, n_job = 0;
+  if (job_ok) seg_job(a, job, p, sigma, begin, n_job);
+
+  SharedConst c;
+  c.sigma = sigma;
+  int cfg = -1;
+  if (job_ok && lane < a.G) cfg = a.group_cfg[(int64_t)p * a.G + lane];
+  if (cfg >= a.C || cfg < 0) cfg = -1;
+  uint64_t hostbits = 0;  // bit m: this lane's group hosts model m
+  if (cfg >= 0) {
+    const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
+    for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> lane) & 1u) << m;
+  }
+  int frow = -1;
+  if (job_ok)
+    for (int f = 0; f < a.n_finish; ++f)
+      if (a.finish_jobs[f] == job) {
+        frow = f;
+        break;
+      }
+  c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
+  c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.finish_stride);
+  c.flimit = n_job < a.finish_stride ? n_job : a.finish_stride;
+  const bool wave_finish = c.fmask != 0;
+  if (wave_finish) __builtin_amdgcn_s_setprio(3);
+  const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
+  const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
+  const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
+  c.lrow = sL + (cfg < 0 ? 0 : cfg) * SMAX;
+  c.lshift = lshift;
+  unsigned char* rec = sR + (size_t)wave * a.M * (1 << RSH);
+  c.rec = rec;
+
+  const int nL = a.M * cp * SMAX;
+  for (int idx = tid; idx < nL; idx += kThreads) {
+    const int s = idx % SMAX;
+    const int mc = idx / SMAX;
+    const int cc = mc % cp;
+    const int m = mc / cp;
+    sL[idx] = (cc < a.C && s < a.cfg_stages[cc])
+                  ? a.stage_lat[((int64_t)m * a.C + cc) * a.smax_in + s]
+                  : 0.0;
+  }
+  for (int m = 0; m < a.M; ++m) {
+    const uint64_t hm = __builtin_amdgcn_ballot_w64((hostbits >> m) & 1u);
+    if (lane == 0) {
+      const uint64_t one = lowest_per_field<W>(hm);
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecMask) = hm;
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount) =
+          one == hm ? 0u : (uint32_t)__builtin_popcountll(one);
+    }
+  }
+  for (int m = lane; m < a.M; m += 64) {
+    unsigned char* r = rec + ((size_t)m << RSH);
+    // this job's SLO of model m: scale * d_single[m] (one rounding)
+    *(double*)(r + rec_slo(SMAX)) = sigma * a.d_single[m];
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s)
+      ((double*)(r + kRecLat))[s] = (uni && s < a.cfg_stages[cfg0])
+                                        ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + s]
+                                        : 0.0;
+  }
+  __syncthreads();
+
+  SharedLane<SMAX> st;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
+  st.fin_sum = st.hash = st.served = 0;
+  st.wlo = 0;
+
+  for (int64_t base = 0; base < n_job; base += kSegChunk) {
+    const int cnt = (int)((n_job - base) < kSegChunk ? (n_job - base) : kSegChunk);
+    // this wavefront's chunk: the previous one has been read (in-order LDS
+    // within a wavefront; the fences keep the compiler from moving accesses)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    for (int e = lane; e < cnt; e += 64) {
+      const double te = a.t[begin + base + e];
+      const uint32_t off = (uint32_t)a.model[begin + base + e] << RSH;
+      const double de = te + *(const double*)(rec + off + rec_slo(SMAX));
+      *(double2*)(sTD + 2 * e) = make_double2(te, de);
+      sO[e] = off;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (uni) {
+      if (wave_finish)
+        fast_chunk<W, SMAX, true, true, true, true>(st, c, sTD, sO, cnt, base, n_job);
+      else
+        fast_chunk<W, SMAX, true, false, true, true>(st, c, sTD, sO, cnt, base, n_job);
+    } else {
+      if (wave_finish)
+        fast_chunk<W, SMAX, true, true, true, false>(st, c, sTD, sO, cnt, base, n_job);
+      else
+        fast_chunk<W, SMAX, true, false, true, false>(st, c, sTD, sO, cnt, base, n_job);
+    }
+  }
+
+  const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum);
+  if (job_ok && lane == 0) {
+    a.out_served[job] = (int64_t)st.served;
+    if (a.out_attain) a.out_attain[job] = n_job > 0 ? (double)st.served / (double)n_job : 0.0;
     if (a.out_digest) {
       a.out_digest[2 * job] = st.hash;
       a.out_digest[2 * job + 1] = fin_sum;
