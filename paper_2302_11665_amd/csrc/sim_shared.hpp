@@ -429,7 +429,7 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
 // segment through its own LDS region -- deadline t + SLO and record offset
 // per request -- with no workgroup barrier in the request loop.
 
-constexpr int kSegChunk = 512;  // requests per staging round of one wavefront
+constexpr int kSegChunk = 256;  // requests per staging round of one wavefront
 
 // LDS bytes of seg_kernel: records, the stage-latency table, and each
 // wavefront's chunk ({t, deadline} pairs, record offsets).
