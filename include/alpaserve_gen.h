@@ -32,6 +32,8 @@ extern "C" {
 #define AS_GEN_PURPOSE_LATENCY 2u  /* model single-device latencies                 */
 #define AS_GEN_PURPOSE_WEIGHT 3u   /* model weight sizes                            */
 #define AS_GEN_PURPOSE_PERMUTE 4u  /* placement permutations (index = candidate id) */
+#define AS_GEN_PURPOSE_WINDOW 5u   /* windowed arrival gaps (index = m * n_windows + w) */
+#define AS_GEN_PURPOSE_WPARAM 6u   /* window parameters of the problem builders      */
 
 /* Stream key for (configuration seed, purpose, index).  Pure function. */
 uint64_t as_gen_key(uint64_t seed, uint64_t purpose, uint64_t index);
@@ -66,6 +68,27 @@ int as_gen_permutations(uint64_t seed, uint64_t purpose, uint64_t first_index, i
 int as_gen_trace(uint64_t seed, int32_t n_models, const double* rate, double cv,
                  double duration, int64_t capacity, double* t_out, int32_t* m_out,
                  int64_t* n_out);
+
+/*
+ * Non-stationary trace: time is cut into n_windows windows of `window`
+ * seconds, and in window w model m receives a Gamma renewal process with its
+ * own rate and CV, restarted at the window's start (Sec. 6.1 fits the
+ * arrivals of each time window of a production trace with a Gamma process
+ * by rate and CV and resamples from the fitted processes; Sec. 6.4 evaluates
+ * placements on a trace other than the one they were chosen for).
+ *   seed        configuration seed; window w of model m uses stream
+ *               as_gen_key(seed, WINDOW, m * n_windows + w)
+ *   rate, cv    [n_models][n_windows] row-major (rate >= 0 finite, 0 = no
+ *               arrivals; cv > 0 finite)
+ *   window      window length in seconds (> 0, finite)
+ * Arrivals of window w are w*window + X_1, + X_2, ... kept while
+ * t < (w + 1)*window (both bounds are one fp64 product).  The per-model
+ * arrival index runs across windows.  Outputs, order and capacity handling
+ * as for as_gen_trace.
+ */
+int as_gen_trace_windowed(uint64_t seed, int32_t n_models, int32_t n_windows, double window,
+                          const double* rate, const double* cv, int64_t capacity, double* t_out,
+                          int32_t* m_out, int64_t* n_out);
 
 #ifdef __cplusplus
 }

@@ -167,6 +167,79 @@ static int gen_model(uint64_t seed, int32_t m, double rate, double cv, double du
   return AS_GEN_OK;
 }
 
+/* Appends one arrival; grows the buffer. */
+static int push_arrival(arrival_t** buf, int64_t* len, int64_t* cap, double t, int32_t m, int64_t j) {
+  if (*len == *cap) {
+    int64_t ncap = *cap ? *cap * 2 : 4096;
+    arrival_t* nb = (arrival_t*)realloc(*buf, (size_t)ncap * sizeof(arrival_t));
+    if (!nb) return AS_GEN_E_NOMEM;
+    *buf = nb;
+    *cap = ncap;
+  }
+  (*buf)[*len].t = t;
+  (*buf)[*len].model = m;
+  (*buf)[*len].idx = j;
+  (*len)++;
+  return AS_GEN_OK;
+}
+
+/* Sort the collected arrivals and copy them out (shared by both traces). */
+static int emit_trace(arrival_t* buf, int64_t len, int64_t capacity, double* t_out, int32_t* m_out,
+                      int64_t* n_out) {
+  *n_out = len;
+  if (len > capacity || (len > 0 && (t_out == NULL || m_out == NULL))) {
+    free(buf);
+    return AS_GEN_E_CAPACITY;
+  }
+  if (len > 0) qsort(buf, (size_t)len, sizeof(arrival_t), cmp_arrival);
+  for (int64_t i = 0; i < len; ++i) {
+    t_out[i] = buf[i].t;
+    m_out[i] = buf[i].model;
+  }
+  free(buf);
+  return AS_GEN_OK;
+}
+
+int as_gen_trace_windowed(uint64_t seed, int32_t n_models, int32_t n_windows, double window,
+                          const double* rate, const double* cv, int64_t capacity, double* t_out,
+                          int32_t* m_out, int64_t* n_out) {
+  if (n_models < 0 || n_windows < 0 || n_out == NULL || capacity < 0) return AS_GEN_E_INVALID_ARG;
+  if (!(window > 0.0) || !isfinite(window)) return AS_GEN_E_INVALID_ARG;
+  const int64_t cells = (int64_t)n_models * n_windows;
+  if (cells > 0 && (rate == NULL || cv == NULL)) return AS_GEN_E_INVALID_ARG;
+  for (int64_t i = 0; i < cells; ++i)
+    if (!(rate[i] >= 0.0) || !isfinite(rate[i]) || !(cv[i] > 0.0) || !isfinite(cv[i]))
+      return AS_GEN_E_INVALID_ARG;
+  arrival_t* buf = NULL;
+  int64_t len = 0, cap = 0;
+  for (int32_t m = 0; m < n_models; ++m) {
+    int64_t j = 0;  /* per-model arrival index, across windows */
+    for (int32_t w = 0; w < n_windows; ++w) {
+      const double r = rate[(int64_t)m * n_windows + w];
+      if (r <= 0.0) continue;
+      const double c = cv[(int64_t)m * n_windows + w];
+      const double shape = 1.0 / (c * c);
+      const double scale = (c * c) / r;
+      const double start = (double)w * window;
+      const double end = (double)(w + 1) * window;
+      const uint64_t key =
+          as_gen_key(seed, AS_GEN_PURPOSE_WINDOW, (uint64_t)m * (uint64_t)n_windows + (uint64_t)w);
+      uint64_t ctr = 0;
+      double t = start;
+      for (;;) {
+        t = t + as_gen_gamma(key, ctr, shape, &ctr) * scale;
+        if (!(t < end)) break;
+        const int rc = push_arrival(&buf, &len, &cap, t, m, j++);
+        if (rc != AS_GEN_OK) {
+          free(buf);
+          return rc;
+        }
+      }
+    }
+  }
+  return emit_trace(buf, len, capacity, t_out, m_out, n_out);
+}
+
 int as_gen_trace(uint64_t seed, int32_t n_models, const double* rate, double cv,
                  double duration, int64_t capacity, double* t_out, int32_t* m_out,
                  int64_t* n_out) {

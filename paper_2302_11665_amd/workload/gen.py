@@ -16,6 +16,8 @@ PURPOSE_ARRIVAL = 1
 PURPOSE_LATENCY = 2
 PURPOSE_WEIGHT = 3
 PURPOSE_PERMUTE = 4
+PURPOSE_WINDOW = 5
+PURPOSE_WPARAM = 6
 
 _lib = None
 
@@ -37,6 +39,11 @@ def _load():
                                      ctypes.c_double, ctypes.c_double, ctypes.c_int64,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         lib.as_gen_trace.restype = ctypes.c_int
+        lib.as_gen_trace_windowed.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p]
+        lib.as_gen_trace_windowed.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -81,6 +88,33 @@ def trace(seed: int, rates, cv: float, duration: float):
             raise ValueError(f"as_gen_trace rc={rc}")
         cap = n.value
     raise RuntimeError("as_gen_trace: capacity retry failed")
+
+
+def trace_windowed(seed: int, rates, cvs, window: float):
+    """Non-stationary trace: rates[m][w], cvs[m][w] per window of `window`
+    seconds.  Returns (t float64[n], model int32[n])."""
+    lib = _load()
+    rates = np.ascontiguousarray(rates, dtype=np.float64)
+    cvs = np.ascontiguousarray(cvs, dtype=np.float64)
+    if rates.ndim != 2 or rates.shape != cvs.shape:
+        raise ValueError("rates and cvs must be [n_models][n_windows] arrays of one shape")
+    if not (np.isfinite(rates).all() and np.isfinite(cvs).all() and math.isfinite(window)):
+        raise ValueError("rates, cvs and window must be finite")
+    M, Wn = rates.shape
+    lam_t = float(rates.sum()) * window
+    cap = int(lam_t + 12.0 * max(float(cvs.max(initial=1.0)), 1.0) * math.sqrt(lam_t + 1.0) + 1024)
+    n = ctypes.c_int64(0)
+    for _ in range(3):
+        t = np.empty(cap, dtype=np.float64)
+        m = np.empty(cap, dtype=np.int32)
+        rc = lib.as_gen_trace_windowed(seed, M, Wn, float(window), rates.ctypes.data, cvs.ctypes.data,
+                                       cap, t.ctypes.data, m.ctypes.data, ctypes.byref(n))
+        if rc == 0:
+            return t[: n.value].copy(), m[: n.value].copy()
+        if rc != -2:
+            raise ValueError(f"as_gen_trace_windowed rc={rc}")
+        cap = n.value
+    raise RuntimeError("as_gen_trace_windowed: capacity retry failed")
 
 
 def traces(specs, threads=None):

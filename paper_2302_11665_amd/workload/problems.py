@@ -274,3 +274,67 @@ def c5_sweep(group_cfg, host_mask, base: Optional[GreedyProblem] = None, n: int 
                         L, gcfg, hm, np.zeros(len(idx), np.int32),
                         np.arange(len(idx), dtype=np.int32), scales, fin,
                         {"grid": n, "points": idx, "configs": used})
+
+
+def window_params(seed: int, base_rates, n_windows: int, sigma: float = 0.5,
+                  cv_lo: float = 1.0, cv_hi: float = 4.0):
+    """Per-window (rate, CV) of a non-stationary workload, a synthetic stand-in
+    for windows fitted to a production trace: model m's log-rate follows a
+    seeded random walk with N(0, sigma^2) steps, centred and clipped to
+    +-2 around log(base_rates[m]); each window's CV is uniform in
+    [cv_lo, cv_hi].  Draws: stream (seed, window-parameter, m), 2 * n_windows
+    uniforms (normals by the inverse normal CDF).  Returns (rates, cvs), both
+    [M][n_windows]."""
+    from scipy.special import ndtri
+    base = np.asarray(base_rates, dtype=np.float64)
+    M = base.shape[0]
+    rates = np.zeros((M, n_windows))
+    cvs = np.zeros((M, n_windows))
+    for m in range(M):
+        u = gen.uniforms(gen.key(seed, gen.PURPOSE_WPARAM, m), 2 * n_windows)
+        walk = np.cumsum(sigma * ndtri(u[:n_windows]))
+        walk = np.clip(walk - walk.mean(), -2.0, 2.0)
+        rates[m] = base[m] * np.exp(walk)
+        cvs[m] = cv_lo + (cv_hi - cv_lo) * u[n_windows:]
+    return rates, cvs
+
+
+@dataclasses.dataclass
+class RobustnessProblem:
+    """One placement search on the assumed trace A, evaluated on trace B
+    (Sec. 6.4: a placement chosen for one slice of traffic serves another)."""
+    greedy: GreedyProblem       # trace A and the partitions to search
+    t_b: np.ndarray
+    model_b: np.ndarray
+    windows: dict
+
+
+def robustness(seed: int = 6, n_models: int = 16, n_devices: int = 16, device_mem_gb: int = 16,
+               n_windows: int = 20, window: float = 60.0, total_rate: float = 64.0,
+               exponent: float = 0.5, slo_scale: float = 5.0,
+               partitions=((4, 4, 1), (4, 2, 2), (8, 8, 1), (16, 4, 4))) -> RobustnessProblem:
+    """Models with d ~ U[0.1, 0.4] s and w ~ U[2, 6] GB; power-law (exponent
+    0.5) base rates summing to total_rate; two non-stationary traces of
+    n_windows windows of `window` seconds with independent window parameters
+    (seeds seed and seed + 1000) -- trace A for the search, trace B for the
+    evaluation."""
+    M = n_models
+    d = _uniform_range(seed, gen.PURPOSE_LATENCY, M, 0.1, 0.4)
+    w = _weights_mib(seed, M, 2.0, 6.0)
+    base = c4_rates(M, total_rate, exponent)
+    ra, ca = window_params(seed, base, n_windows)
+    rb, cb = window_params(seed + 1000, base, n_windows)
+    ta, ma = gen.trace_windowed(seed, ra, ca, window)
+    tb, mb = gen.trace_windowed(seed + 1000, rb, cb, window)
+    cfgs = [(S, k) for _, S, k in partitions]
+    L = stage_table(d, cfgs)
+    parts = []
+    for c, (size, S, k) in enumerate(partitions):
+        G = n_devices // size
+        parts.append({"group_cfg": np.full(G, c, np.int32),
+                      "group_mem_mib": np.full(G, size * device_mem_gb * GIB_MIB, np.int64),
+                      "label": f"{G}x(S={S},k={k})"})
+    gp = GreedyProblem("robustness_a", ta, ma, d, w, np.array([S for S, _ in cfgs], np.int32),
+                       np.array([k for _, k in cfgs], np.int32), L, parts, slo_scale,
+                       {"devices": n_devices, "device_mem_mib": device_mem_gb * GIB_MIB})
+    return RobustnessProblem(gp, tb, mb, {"a": (ra, ca), "b": (rb, cb), "window": window})

@@ -37,6 +37,9 @@ def golden_traces():
     out.append(("c3_trace_120s", t, m))
     t, m = gen.trace(5000 + 273, [4.0 * 0.25 * 16.0 ** (1 / 15)] * 32, 8.0 ** (1 / 15), 600.0)
     out.append(("c5_point273", t, m))
+    r, c = problems.window_params(6, problems.c4_rates(16, 64.0, 0.5), 20)
+    t, m = gen.trace_windowed(6, r, c, 60.0)
+    out.append(("robustness_trace_a", t, m))
     return out
 
 
@@ -131,3 +134,85 @@ def test_problem_shapes():
     assert pb2.n_jobs == 512
     assert np.all((pb2.weight_mib >= 2048) & (pb2.weight_mib < 6144))
     assert np.all((pb2.d_single >= 0.1) & (pb2.d_single < 0.4))
+
+
+# ---------------------------------------------------------------- windowed
+# Non-stationary traces (Sec. 6.1 fits each time window of a production trace
+# with a Gamma process by rate and CV; Sec. 6.4 evaluates on another slice).
+
+def _window_arrivals(t, m, model, w, window):
+    return t[(m == model) & (t >= w * window) & (t < (w + 1) * window)]
+
+
+def test_windowed_bounds_counts_and_cv():
+    """Every arrival lies in its window; per window the count matches
+    rate * window (Gamma renewal count: variance about rate*window*CV^2) and
+    the gaps inside the window have the window's CV."""
+    window = 2000.0
+    rates = np.array([[3.0, 0.0, 10.0], [1.0, 6.0, 2.0]])
+    cvs = np.array([[1.0, 2.0, 3.0], [0.5, 4.0, 1.5]])
+    t, m = gen.trace_windowed(11, rates, cvs, window)
+    assert np.all(np.diff(t) >= 0)
+    assert np.all((t >= 0) & (t < 3 * window))
+    for mm in range(2):
+        for w in range(3):
+            a = _window_arrivals(t, m, mm, w, window)
+            lam, cv = rates[mm, w], cvs[mm, w]
+            if lam == 0.0:
+                assert len(a) == 0
+                continue
+            mean = lam * window
+            sd = math.sqrt(mean) * cv
+            assert abs(len(a) - mean) < 5 * sd + 5, (mm, w, len(a), mean)
+            gaps = np.diff(np.concatenate([[w * window], a]))
+            est = gaps.std() / gaps.mean()
+            assert abs(est - cv) < 0.12 * cv + 0.05, (mm, w, est, cv)
+    # arrivals of model 0 across all windows: counted once each
+    assert (m == 0).sum() == sum(len(_window_arrivals(t, m, 0, w, window)) for w in range(3))
+
+
+def test_windowed_streams_are_per_window():
+    """Changing one (model, window) cell leaves every other cell's arrivals
+    bit-identical (each cell draws from its own stream)."""
+    window = 100.0
+    rates = np.full((3, 4), 2.0)
+    cvs = np.full((3, 4), 2.0)
+    t0, m0 = gen.trace_windowed(5, rates, cvs, window)
+    rates2 = rates.copy()
+    rates2[1, 2] = 7.0
+    t1, m1 = gen.trace_windowed(5, rates2, cvs, window)
+    for mm in range(3):
+        for w in range(4):
+            a = _window_arrivals(t0, m0, mm, w, window)
+            b = _window_arrivals(t1, m1, mm, w, window)
+            if (mm, w) == (1, 2):
+                assert len(b) > len(a)
+            else:
+                assert a.tobytes() == b.tobytes(), (mm, w)
+
+
+def test_windowed_deterministic_and_rejects_bad_args():
+    rates = np.array([[1.0, 2.0]])
+    cvs = np.array([[1.0, 3.0]])
+    a = gen.trace_windowed(3, rates, cvs, 50.0)
+    b = gen.trace_windowed(3, rates, cvs, 50.0)
+    assert a[0].tobytes() == b[0].tobytes() and a[1].tobytes() == b[1].tobytes()
+    for r, c, w in [([[-1.0, 1.0]], cvs, 50.0), (rates, [[0.0, 1.0]], 50.0), (rates, cvs, 0.0),
+                    ([[np.inf, 1.0]], cvs, 50.0)]:
+        with pytest.raises(ValueError):
+            gen.trace_windowed(3, np.array(r), np.array(c), w)
+    t, m = gen.trace_windowed(3, np.zeros((2, 0)), np.zeros((2, 0)), 10.0)
+    assert len(t) == 0
+
+
+def test_window_params_recipe():
+    base = np.array([4.0, 1.0, 0.5])
+    r, c = problems.window_params(9, base, 50)
+    assert r.shape == (3, 50) and c.shape == (3, 50)
+    assert np.all(c >= 1.0) and np.all(c <= 4.0)
+    # log-rate centred on the base and clipped to +-2
+    lr = np.log(r / base[:, None])
+    assert np.all(np.abs(lr) <= 2.0 + 1e-12)
+    assert np.all(np.abs(lr.mean(axis=1)) < 0.5)
+    r2, _ = problems.window_params(9, base, 50)
+    assert np.array_equal(r, r2)
