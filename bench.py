@@ -36,21 +36,25 @@ METRIC = "simulated request×placement events/sec on 1 GPU; % of HBM/VALU roofli
 PEAK_FP64_OPS = 256 * 4 * 16 * 2.4e9
 HBM_PEAK = 8.0e12
 
-# HBM traffic of one launch of the simulator kernel on the default workload:
-# rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by
-# what the same counter reads for a plain 1 GiB device copy (FETCH_SIZE reads
-# 524300.75 KiB for 1048576 KiB fetched, WRITE_SIZE exactly 1048576 KiB).  The
-# figures belong to the kernel sources whose SHA-256 is recorded here; once
-# those change, traffic is reported as null until it is measured again.
+# HBM traffic of one launch of the simulator kernels: rocprofv3 --pmc
+# FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what the same
+# counter reads for a plain 1 GiB device copy.  The figures belong to the
+# kernel sources (and compile flags) whose SHA-256 is recorded here; once those
+# change, traffic is reported as null until it is measured again.
 KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd/csrc/sim_kernel.hpp",
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
-                  "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/build.py",
-                  "include/alpaserve_sim.h"]
+                  "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_internal.hpp"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "3a616b6811e88f35d3ff1a2241284ac905177067e18c61c0ebf0a249fc35f888",
+    "sources_sha256": "e250e1b629735ddc321826e744c878ee5fb5e8c938f0a2692de1bc42bc96e85b",
     "kernel": "shared_kernel<16, 4, true>",
-    "fetch_kib": 327513.7, "write_kib": 450111.0,
-    "fetch_scale": 1048576.0 / 524300.75, "write_scale": 1.0,
+    "fetch_kib": 327576.3125, "write_kib": 450111.0,
+    "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
+}
+MEASURED_TRAFFIC_SWEEP = {
+    "sources_sha256": "e250e1b629735ddc321826e744c878ee5fb5e8c938f0a2692de1bc42bc96e85b",
+    "kernel": "seg_kernel<1>",
+    "fetch_kib": 2595204.0, "write_kib": 13847.75,
+    "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 
 
@@ -78,18 +82,20 @@ def algorithmic_ops(pb):
 
 
 def sources_sha256():
+    """SHA-256 over the kernel sources and the HIP compile flags."""
     import hashlib
+    from paper_2302_11665_amd import build
     h = hashlib.sha256()
     for f in sorted(KERNEL_SOURCES):
         h.update(os.path.basename(f).encode())
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
+    h.update(" ".join(build.HIP_FLAGS).encode())
     return h.hexdigest()
 
 
-def measured_traffic(default_workload):
-    m = MEASURED_TRAFFIC
-    if not default_workload or sources_sha256() != m["sources_sha256"]:
+def measured_traffic(m, default_workload):
+    if not default_workload or m["sources_sha256"] is None or sources_sha256() != m["sources_sha256"]:
         return None
     return round((m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024.0)
 
@@ -155,7 +161,7 @@ def bench_sweep(args, np, torch, api, problems):
             "jobs": int(len(sp.job_segment)), "requests": int(len(sp.t)), "events": int(events),
             "ms_per_step": round(ms, 3), "value": round(events / (ms / 1000.0), 1), "unit": "events/s",
             "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-                         "frac": round(gbs * 1e9 / HBM_PEAK, 5), "traffic": None,
+                         "frac": round(gbs * 1e9 / HBM_PEAK, 5), "traffic": measured_traffic(MEASURED_TRAFFIC_SWEEP, True),
                          "algorithmic_bytes": int(nbytes)},
             "served_total": int(res["served"].sum()),
             "trace_gen_s": round(gen_s, 3), "upload_s": round(up_s, 3)}
@@ -239,7 +245,7 @@ def main():
     peak = PEAK_FP64_OPS / 1e12
     roof = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(peak, 2), "unit": "TFLOP/s",
             "frac": round(achieved / peak, 5),
-            "traffic": measured_traffic(args.placements == 8192 and args.duration == 3600.0),
+            "traffic": measured_traffic(MEASURED_TRAFFIC, args.placements == 8192 and args.duration == 3600.0),
             "algorithmic_bytes": int(algorithmic_bytes(pb)),
             "ops_per_event": round(ops / events, 3),
             "note": "fp64 lane-ops (max/add/cmp/mul, no FMA) of the definition per launch / mean launch time"}

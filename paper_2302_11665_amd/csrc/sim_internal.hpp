@@ -1,0 +1,28 @@
+// Host-side helpers of the C-ABI shared by its translation units (checks,
+// error reporting, the shared-trace launch).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "alpaserve_sim.h"
+#include "sim_kernel.hpp"
+
+namespace as_host {
+
+using as_dev::KArgs;
+
+// Record a message for as_last_error() and return code.
+int fail(int code, const char* fmt, ...);
+// Clear the message and return AS_OK.
+int ok();
+int pow2ceil(int x);
+// Checks shared by the simulate entry points; fill the model and placement
+// part of a (placement arrays may be set later by the caller) and return the
+// group count in W and the padded stage count in smax.
+int check_common(const as_models_t* models, const as_placements_t* plc, KArgs& a, int& W, int& smax);
+// Launch the batched simulation of a shared trace; a is complete except for
+// the kernel shape, W is the group count on entry.
+int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream);
+
+}  // namespace as_host
