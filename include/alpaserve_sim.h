@@ -181,8 +181,46 @@ int as_greedy_placement(const as_trace_t* trace, const as_models_t* models,
                         void* stream);
 
 /*
+ * Alg. 1 with beam size `beam` >= 1 (Sec. 4.2): every step expands each
+ * selection of the beam, in beam order, by every feasible (m, g) addition in
+ * (m, g) order, drops a new selection equal to one produced earlier in the
+ * same step, scores all of them in one batched launch, keeps the `beam` most
+ * served (the earlier candidate first on ties) as the next beam and compares
+ * the best of them with the best selection so far (replaced only by a
+ * strictly better one).  Arguments as for as_greedy_placement (beam = 1 is
+ * as_greedy_placement); step i records the best selection of step i: the
+ * replica (step_model, step_group) that its parent gained and its served
+ * count.
+ */
+int as_beam_placement(const as_trace_t* trace, const as_models_t* models, const int64_t* weight_mib,
+                      int32_t n_groups, const int32_t* group_cfg, const int64_t* group_mem_mib,
+                      double slo_scale, int32_t beam, uint64_t* best_mask, int64_t* best_served,
+                      int32_t* step_model, int32_t* step_group, int64_t* step_served, int32_t max_steps,
+                      int32_t* n_steps, void* stream);
+
+/*
+ * The fast heuristic of Sec. 4.2 for very large workloads: simulate the
+ * current selection once (as_simulate_stats), then add the model with the
+ * most unserved requests (its requests in the trace minus the served ones;
+ * among models that still fit on some group; lowest id on ties) to the
+ * available group with the lowest utilization (least busy time; among the
+ * groups where the replica fits; lowest index on ties); repeat until no
+ * replica fits.  Every simulated selection, the last one included, competes
+ * for the result (replaced only by a strictly better one).  Arguments as for
+ * as_greedy_placement; step i records the replica added and the served count
+ * of the selection it was added to.
+ */
+int as_fast_placement(const as_trace_t* trace, const as_models_t* models, const int64_t* weight_mib,
+                      int32_t n_groups, const int32_t* group_cfg, const int64_t* group_mem_mib,
+                      double slo_scale, uint64_t* best_mask, int64_t* best_served, int32_t* step_model,
+                      int32_t* step_group, int64_t* step_served, int32_t max_steps, int32_t* n_steps,
+                      void* stream);
+
+/*
  * Reduced Alg. 2 (Sec. 4.2): run as_greedy_placement on each of n_partitions
- * partitions and keep the strictly best (first on ties).  Partition p has
+ * partitions and keep the strictly best (first on ties).  The partitions'
+ * searches advance in lockstep: one launch per step scores the candidates of
+ * all of them.  Partition p has
  * part_groups[p] groups whose configurations and memories are
  * part_cfg[off_p ..] and part_mem_mib[off_p ..], off_p = sum of earlier
  * part_groups (HOST arrays).  Outputs: *best_partition, best_mask[M] (HOST),
@@ -193,6 +231,31 @@ int as_partition_search(const as_trace_t* trace, const as_models_t* models,
                         const int32_t* part_cfg, const int64_t* part_mem_mib, double slo_scale,
                         int32_t* best_partition, uint64_t* best_mask, int64_t* best_served,
                         int64_t* part_served, void* stream);
+
+/*
+ * The simulation of as_simulate_placements with the statistics that the fast
+ * placement heuristic of Sec. 4.2 reads after simulating a selection once
+ * (place the model with the most unserved requests on the available group
+ * with the lowest utilization).  Jobs and scales as for
+ * as_simulate_placements (job j = p * K + k); every pointer is a device
+ * pointer.
+ *   out_served[J]             served counts (required)
+ *   out_digest[J][2]          {h, fin_sum} as above, or NULL
+ *   out_model_served[J][M]    served requests of each model, or NULL
+ *   out_group_busy[J][G]      busy time of each group, or NULL: for every
+ *                             request group g serves, in trace order, the
+ *                             largest stage latency of that model in g's
+ *                             configuration (the stage that bounds the
+ *                             group's throughput, Sec. 3.4) is added to an
+ *                             fp64 sum starting at 0
+ * One job per wavefront (lane = group); meant for few jobs per call.  The
+ * stage-latency table must fit in the LDS of a workgroup (AS_E_LIMITS
+ * otherwise).
+ */
+int as_simulate_stats(const as_trace_t* trace, const as_models_t* models,
+                      const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
+                      int64_t* out_served, uint64_t* out_digest, int64_t* out_model_served,
+                      double* out_group_busy, void* stream);
 
 /* Message of the last failed call on this thread ("" if none); valid until
  * the next call on this thread. */

@@ -56,6 +56,11 @@ class OracleLib:
                       ctypes.c_int32, P, ctypes.c_int32, P, P, ctypes.c_double, P, P, P]
         f.restype = ctypes.c_int
         self._fn = f
+        g = getattr(self._lib, "oracle_simulate_job_stats", None)
+        if g is not None:
+            g.argtypes = f.argtypes + [P, P]
+            g.restype = ctypes.c_int
+        self._fn_stats = g
 
     def simulate_job(self, t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
                      slo_scale, want_finish=False):
@@ -86,6 +91,33 @@ class OracleLib:
         if rc != 0:
             raise ValueError(f"oracle_simulate_job rejected its arguments (rc={rc})")
         return int(served[0]), (int(digest[0]), int(digest[1])), finish
+
+    def simulate_job_stats(self, t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
+                           slo_scale):
+        """simulate_job plus the fast heuristic's statistics.  Returns (served,
+        (h, fin_sum), model_served int64[M], group_busy float64[G])."""
+        t = np.ascontiguousarray(t, dtype=np.float64)
+        model = np.ascontiguousarray(model, dtype=np.int32)
+        d_single = np.ascontiguousarray(d_single, dtype=np.float64)
+        cfg_stages = np.ascontiguousarray(cfg_stages, dtype=np.int32)
+        stage_lat = np.ascontiguousarray(stage_lat, dtype=np.float64)
+        group_cfg = np.ascontiguousarray(group_cfg, dtype=np.int32)
+        host_mask = np.ascontiguousarray(host_mask, dtype=np.uint64)
+        n = t.shape[0]
+        M, C, S = stage_lat.shape
+        G = group_cfg.shape[0]
+        served = np.zeros(1, dtype=np.int64)
+        digest = np.zeros(2, dtype=np.uint64)
+        ms = np.zeros(M, dtype=np.int64)
+        busy = np.zeros(G, dtype=np.float64)
+        rc = self._fn_stats(n, t.ctypes.data, model.ctypes.data, M, d_single.ctypes.data, C,
+                            cfg_stages.ctypes.data, S, stage_lat.ctypes.data, G,
+                            group_cfg.ctypes.data, host_mask.ctypes.data, float(slo_scale),
+                            served.ctypes.data, digest.ctypes.data, None, ms.ctypes.data,
+                            busy.ctypes.data)
+        if rc != 0:
+            raise ValueError(f"oracle_simulate_job_stats rejected its arguments (rc={rc})")
+        return int(served[0]), (int(digest[0]), int(digest[1])), ms, busy
 
     def simulate_placements(self, t, model, d_single, cfg_stages, stage_lat, group_cfg,
                             host_mask, slo_scale, finish_jobs=(), threads=None):

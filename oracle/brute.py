@@ -73,15 +73,19 @@ def _replay(requests, lat_rows):
     return depart
 
 
-def simulate(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale):
+def simulate(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
+             return_groups=False):
     """Simulate one job.  Returns (served, finish[n]) with finish = departure time
-    of accepted requests, -1.0 for rejected and -2.0 for unhosted models."""
+    of accepted requests, -1.0 for rejected and -2.0 for unhosted models; with
+    return_groups, also group[n]: the group the controller chose for each
+    request (-1 when no group hosts the model)."""
     t = [float(x) for x in t]
     model = [int(x) for x in model]
     n = len(t)
     G = len(group_cfg)
     admitted = {g: ([], []) for g in range(G)}  # g -> (arrival times, latency rows)
     finish = np.empty(n, dtype=np.float64)
+    chosen = np.full(n, -1, dtype=np.int64)
     served = 0
     for i in range(n):
         m, a = model[i], t[i]
@@ -96,6 +100,7 @@ def simulate(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, sl
             key = dep[-1][0] if dep else 0.0
             if best is None or key < best_key:
                 best, best_key = g, key
+        chosen[i] = best
         c = int(group_cfg[best])
         S = int(cfg_stages[c])
         row = [float(stage_lat[m][c][s]) for s in range(S)]
@@ -110,4 +115,6 @@ def simulate(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, sl
             rows.append(row)
             finish[i] = f
             served += 1
+    if return_groups:
+        return served, finish, chosen
     return served, finish

@@ -76,11 +76,24 @@ static uint64_t bits_of(double x) {
  *   slo_scale               SLO multiple of d_single
  * Outputs: *served_out, digest_out[2] = {h, fin_sum}, finish_out[n] (may be NULL).
  */
-int oracle_simulate_job(int64_t n, const double* t, const int32_t* model, int32_t n_models,
-                        const double* d_single, int32_t n_configs, const int32_t* cfg_stages,
-                        int32_t max_stages, const double* stage_lat, int32_t n_groups,
-                        const int32_t* group_cfg, const uint64_t* host_mask, double slo_scale,
-                        int64_t* served_out, uint64_t* digest_out, double* finish_out) {
+/*
+ * The same simulation with two more outputs, for the fast placement
+ * heuristic of Sec. 4.2 (simulate once, then place the model with the most
+ * unserved requests on the available group with the lowest utilization):
+ *   model_served_out[n_models]  served requests of each model (may be NULL)
+ *   group_busy_out[n_groups]    busy time of each group: for every request the
+ *                               group serves, in trace order, the latency of
+ *                               its slowest stage for that model (the stage
+ *                               that bounds the group's throughput, Sec. 3.4)
+ *                               is added to a running fp64 sum; 0 for groups
+ *                               that serve nothing (may be NULL)
+ */
+int oracle_simulate_job_stats(int64_t n, const double* t, const int32_t* model, int32_t n_models,
+                              const double* d_single, int32_t n_configs, const int32_t* cfg_stages,
+                              int32_t max_stages, const double* stage_lat, int32_t n_groups,
+                              const int32_t* group_cfg, const uint64_t* host_mask, double slo_scale,
+                              int64_t* served_out, uint64_t* digest_out, double* finish_out,
+                              int64_t* model_served_out, double* group_busy_out) {
   if (n < 0 || n_models <= 0 || n_configs <= 0 || max_stages <= 0 || n_groups <= 0 ||
       n_groups > 64 || !served_out || !digest_out)
     return ORACLE_E_ARG;
@@ -105,6 +118,10 @@ int oracle_simulate_job(int64_t n, const double* t, const int32_t* model, int32_
     if (model[i] < 0 || model[i] >= n_models) goto bad_arg;
 
   for (int32_t m = 0; m < n_models; ++m) slo[m] = slo_scale * d_single[m];
+  if (model_served_out)
+    for (int32_t m = 0; m < n_models; ++m) model_served_out[m] = 0;
+  if (group_busy_out)
+    for (int32_t g = 0; g < n_groups; ++g) group_busy_out[g] = 0.0;
 
   int64_t served = 0;
   uint64_t h = 0, word = 0, fin_sum = 0;
@@ -137,6 +154,13 @@ int oracle_simulate_job(int64_t n, const double* t, const int32_t* model, int32_
         out = -1.0;
       } else {
         for (int32_t s = 0; s < S; ++s) F[gs * max_stages + s] = f[s];
+        if (model_served_out) model_served_out[m] += 1;
+        if (group_busy_out) {
+          double slowest = 0.0;
+          for (int32_t s = 0; s < S; ++s)
+            slowest = oracle_max(slowest, stage_lat[((int64_t)m * n_configs + c) * max_stages + s]);
+          group_busy_out[gs] += slowest;
+        }
         served += 1;
         fin_sum += bits_of(prev);
         word |= (uint64_t)1 << (i & 63);
@@ -162,4 +186,14 @@ bad_arg:
   free(slo);
   free(f);
   return ORACLE_E_ARG;
+}
+
+int oracle_simulate_job(int64_t n, const double* t, const int32_t* model, int32_t n_models,
+                        const double* d_single, int32_t n_configs, const int32_t* cfg_stages,
+                        int32_t max_stages, const double* stage_lat, int32_t n_groups,
+                        const int32_t* group_cfg, const uint64_t* host_mask, double slo_scale,
+                        int64_t* served_out, uint64_t* digest_out, double* finish_out) {
+  return oracle_simulate_job_stats(n, t, model, n_models, d_single, n_configs, cfg_stages, max_stages,
+                                   stage_lat, n_groups, group_cfg, host_mask, slo_scale, served_out,
+                                   digest_out, finish_out, NULL, NULL);
 }

@@ -17,6 +17,8 @@ int fail(int code, const char* fmt, ...);
 // Clear the message and return AS_OK.
 int ok();
 int pow2ceil(int x);
+// LDS a workgroup may use on the current device (160 KiB on gfx950).
+size_t shared_lds_limit();
 // Checks shared by the simulate entry points; fill the model and placement
 // part of a (placement arrays may be set later by the caller) and return the
 // group count in W and the padded stage count in smax.

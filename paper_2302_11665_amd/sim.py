@@ -83,6 +83,16 @@ def lib():
         L.as_partition_search.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t), _P,
                                           ctypes.c_int32, _P, _P, _P, ctypes.c_double, _P, _P, _P, _P, _P]
         L.as_partition_search.restype = ctypes.c_int
+        L.as_beam_placement.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t), _P,
+                                        ctypes.c_int32, _P, _P, ctypes.c_double, ctypes.c_int32, _P, _P,
+                                        _P, _P, _P, ctypes.c_int32, _P, _P]
+        L.as_beam_placement.restype = ctypes.c_int
+        L.as_fast_placement.argtypes = L.as_greedy_placement.argtypes
+        L.as_fast_placement.restype = ctypes.c_int
+        L.as_simulate_stats.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t),
+                                        ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, _P, _P, _P,
+                                        _P, _P]
+        L.as_simulate_stats.restype = ctypes.c_int
         L.as_last_error.argtypes = []
         L.as_last_error.restype = ctypes.c_char_p
         L.as_version.argtypes = []
@@ -213,6 +223,12 @@ def as_greedy_placement(t, model, d_single, cfg_stages, stage_lat, weight_mib, g
                         slo_scale, max_steps=4096, stream=None):
     """Marshal to as_greedy_placement (device trace/model tables, host
     partition).  Returns dict(best_mask uint64[M], best_served, steps=[(m, g, served)])."""
+    return _search_call(lib().as_greedy_placement, (), t, model, d_single, cfg_stages, stage_lat,
+                        weight_mib, group_cfg, group_mem_mib, slo_scale, max_steps, stream)
+
+
+def _search_call(fn, extra, t, model, d_single, cfg_stages, stage_lat, weight_mib, group_cfg,
+                 group_mem_mib, slo_scale, max_steps, stream):
     tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
     md, _keep = make_models(d_single, cfg_stages, stage_lat)
     M = md.n_models
@@ -225,14 +241,43 @@ def as_greedy_placement(t, model, d_single, cfg_stages, stage_lat, weight_mib, g
     sg = np.zeros(max_steps, dtype=np.int32)
     ss = np.zeros(max_steps, dtype=np.int64)
     n = np.zeros(1, dtype=np.int32)
-    rc = lib().as_greedy_placement(ctypes.byref(tr), ctypes.byref(md), w.ctypes.data, int(gc.shape[0]),
-                                   gc.ctypes.data, gm.ctypes.data, float(slo_scale), best.ctypes.data,
-                                   best_s.ctypes.data, sm.ctypes.data, sg.ctypes.data, ss.ctypes.data,
-                                   max_steps, n.ctypes.data, _stream(stream))
+    rc = fn(ctypes.byref(tr), ctypes.byref(md), w.ctypes.data, int(gc.shape[0]), gc.ctypes.data,
+            gm.ctypes.data, float(slo_scale), *extra, best.ctypes.data, best_s.ctypes.data, sm.ctypes.data,
+            sg.ctypes.data, ss.ctypes.data, max_steps, n.ctypes.data, _stream(stream))
     _check(rc)
     k = min(int(n[0]), max_steps)
     return {"best_mask": best, "best_served": int(best_s[0]), "n_steps": int(n[0]),
             "steps": [(int(sm[i]), int(sg[i]), int(ss[i])) for i in range(k)]}
+
+
+def as_beam_placement(t, model, d_single, cfg_stages, stage_lat, weight_mib, group_cfg, group_mem_mib,
+                      slo_scale, beam, max_steps=4096, stream=None):
+    """Marshal to as_beam_placement.  Returns dict(best_mask, best_served, n_steps,
+    steps=[(m, g, served)] of each step's best selection)."""
+    return _search_call(lib().as_beam_placement, (int(beam),), t, model, d_single, cfg_stages, stage_lat,
+                        weight_mib, group_cfg, group_mem_mib, slo_scale, max_steps, stream)
+
+
+def as_fast_placement(t, model, d_single, cfg_stages, stage_lat, weight_mib, group_cfg, group_mem_mib,
+                      slo_scale, max_steps=4096, stream=None):
+    """Marshal to as_fast_placement.  Returns dict(best_mask, best_served, n_steps,
+    steps=[(m, g, served before the addition)])."""
+    return _search_call(lib().as_fast_placement, (), t, model, d_single, cfg_stages, stage_lat,
+                        weight_mib, group_cfg, group_mem_mib, slo_scale, max_steps, stream)
+
+
+def as_simulate_stats(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
+                      out_served, out_digest=None, out_model_served=None, out_group_busy=None,
+                      stream=None):
+    """Marshal to as_simulate_stats (device tensors as for as_simulate_placements;
+    out_model_served[P*K, M] i64, out_group_busy[P*K, G] f64)."""
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    pl = make_placements(group_cfg, host_mask)
+    rc = lib().as_simulate_stats(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl), _ptr(slo_scale),
+                                 int(slo_scale.shape[0]), _ptr(out_served), _ptr(out_digest),
+                                 _ptr(out_model_served), _ptr(out_group_busy), _stream(stream))
+    _check(rc)
 
 
 def as_partition_search(t, model, d_single, cfg_stages, stage_lat, weight_mib, partitions, slo_scale,

@@ -114,3 +114,46 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(sim.as_models_t) == 40
     assert ctypes.sizeof(sim.as_placements_t) == 24
     assert ctypes.sizeof(sim.as_job_t) == 16
+
+
+def test_search_and_stats_argument_errors(L):
+    """Beam search, fast heuristic and statistics reject bad arguments before
+    any device work."""
+    md, _k = _models(M=2)
+    tr = sim.as_trace_t(4, 0x10, 0x20)
+    w = np.array([1, 2], np.int64)
+    gc = np.array([0, 0], np.int32)
+    gm = np.array([10, 10], np.int64)
+    best = np.zeros(2, np.uint64)
+    bs = np.zeros(1, np.int64)
+    n = np.zeros(1, np.int32)
+
+    def beam(k, trace=tr, G=2, scale=1.0, weights=w):
+        return L.as_beam_placement(ctypes.byref(trace) if trace is not None else None, ctypes.byref(md),
+                                   weights.ctypes.data, G, gc.ctypes.data, gm.ctypes.data, scale, k,
+                                   best.ctypes.data, bs.ctypes.data, None, None, None, 0, n.ctypes.data, None)
+
+    def fast(trace=tr, G=2, scale=1.0):
+        return L.as_fast_placement(ctypes.byref(trace) if trace is not None else None, ctypes.byref(md),
+                                   w.ctypes.data, G, gc.ctypes.data, gm.ctypes.data, scale,
+                                   best.ctypes.data, bs.ctypes.data, None, None, None, 0, n.ctypes.data, None)
+
+    assert beam(0) == sim.AS_E_INVALID_ARG
+    assert "beam" in sim.as_last_error()
+    assert beam(2, trace=None) == sim.AS_E_INVALID_ARG
+    assert beam(2, G=0) == sim.AS_E_LIMITS
+    assert beam(2, G=65) == sim.AS_E_LIMITS
+    assert beam(2, scale=float("nan")) == sim.AS_E_INVALID_ARG
+    assert beam(2, weights=np.array([1, -1], np.int64)) == sim.AS_E_INVALID_ARG
+    assert fast(trace=None) == sim.AS_E_INVALID_ARG
+    assert fast(G=0) == sim.AS_E_LIMITS
+    assert fast(scale=-1.0) == sim.AS_E_INVALID_ARG
+    pl = sim.as_placements_t(3, 4, 0x30, 0x40)
+    st = L.as_simulate_stats
+    assert st(None, ctypes.byref(md), ctypes.byref(pl), 0x50, 1, 0x60, None, None, None, None) == sim.AS_E_INVALID_ARG
+    assert st(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl), None, 1, 0x60, None, None, None,
+              None) == sim.AS_E_INVALID_ARG
+    assert st(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl), 0x50, -1, 0x60, None, None, None,
+              None) == sim.AS_E_INVALID_ARG
+    assert st(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(sim.as_placements_t(0, 4, None, None)), 0x50, 1,
+              None, None, None, None, None) == sim.AS_OK

@@ -37,8 +37,8 @@ MUTANTS = {
     "commit_when_rejected": ("if (prev > deadline) {\n        out = -1.0;",
                              "for (int32_t s = 0; s < S; ++s) F[gs * max_stages + s] = f[s];\n"
                              "      if (prev > deadline) {\n        out = -1.0;"),
-    "update_stage0_only": ("for (int32_t s = 0; s < S; ++s) F[gs * max_stages + s] = f[s];\n        served",
-                           "F[gs * max_stages + 0] = f[0];\n        served"),
+    "update_stage0_only": ("for (int32_t s = 0; s < S; ++s) F[gs * max_stages + s] = f[s];\n        if (model_served_out)",
+                           "F[gs * max_stages + 0] = f[0];\n        if (model_served_out)"),
     "slo_additive": ("slo[m] = slo_scale * d_single[m];", "slo[m] = slo_scale + d_single[m];"),
     "deadline_from_free_time": ("const double deadline = ti + slo[m];",
                                 "const double deadline = F[gs * max_stages + 0] + slo[m];"),
