@@ -257,6 +257,73 @@ int as_simulate_stats(const as_trace_t* trace, const as_models_t* models,
                       int64_t* out_served, uint64_t* out_digest, int64_t* out_model_served,
                       double* out_group_busy, void* stream);
 
+#define AS_MAX_BUCKETS 8 /* model buckets of one placement (Alg. 2) */
+
+/* Options of as_placement_search (Alg. 2).  HOST struct. */
+typedef struct {
+  int32_t n_devices;          /* devices of the cluster, a multiple of device_unit        */
+  int32_t device_unit;        /* device counts of buckets are multiples of this, >= 1     */
+  int64_t device_mem_mib;     /* memory of one device (MiB), >= 0                         */
+  const int32_t* cfg_devices; /* HOST [C] devices of a group of configuration c (S_c*k_c) */
+  double bucket_threshold;    /* largest latency span (s) inside a model bucket, >= 0     */
+  double balance_ratio;       /* largest max/min ratio of bucket loads kept, >= 1 (+inf:
+                                 keep every split)                                         */
+  double slo_scale;           /* SLO multiple of d_single for every model, >= 0           */
+  int32_t max_buckets;        /* 1..AS_MAX_BUCKETS                                        */
+  int32_t beam;               /* Alg. 1 beam size (>= 1), or 0 for the fast heuristic     */
+} as_search_opts_t;
+
+/* Result of as_placement_search.  HOST struct, written by the call.  Bucket b
+ * has bucket_groups[b] groups with configurations bucket_group_cfg[b][0..],
+ * each holding (number of its devices) x device_mem_mib MiB; bit g of
+ * bucket_mask[b][m] is set iff its group g hosts model m. */
+typedef struct {
+  int64_t served;                 /* requests the placement serves (sum over buckets)  */
+  int32_t n_buckets;              /* 0 when no placement serves anything               */
+  int32_t n_bucket_configs;       /* model-bucket cuts enumerated                      */
+  int32_t n_device_splits;        /* device splits enumerated                          */
+  int32_t n_kept_splits;          /* splits kept by the balance rule                   */
+  int32_t n_problems;             /* Alg. 1 problems solved (bucket x devices x config) */
+  int32_t model_bucket[AS_MAX_MODELS];                 /* bucket of each model       */
+  int32_t bucket_devices[AS_MAX_BUCKETS];              /* devices of each bucket     */
+  int32_t bucket_cfg[AS_MAX_BUCKETS];                  /* configuration of its equal
+                                                          groups; -1 if it serves nothing */
+  int32_t bucket_groups[AS_MAX_BUCKETS];
+  int32_t bucket_group_cfg[AS_MAX_BUCKETS][AS_MAX_GROUPS];
+  int64_t bucket_served[AS_MAX_BUCKETS];
+  uint64_t bucket_mask[AS_MAX_BUCKETS][AS_MAX_MODELS];
+} as_search_result_t;
+
+/*
+ * Alg. 2 of Sec. 4.2: enumerate model buckets, device buckets, group
+ * partitions and parallel configurations, run Alg. 1 (beam >= 1) or the fast
+ * heuristic (beam = 0) for every bucket option, keep each bucket's strictly
+ * best option and the strictly best concatenation (first on ties; the empty
+ * placement serves 0).
+ *   model buckets   models sorted by d_single (ties by id) cut into 1..
+ *                   max_buckets contiguous runs, each spanning at most
+ *                   bucket_threshold seconds (every such cut is tried)
+ *   device buckets  every split of n_devices into the buckets in multiples
+ *                   of device_unit (lexicographic), dropped when the largest
+ *                   bucket load exceeds balance_ratio times the smallest; a
+ *                   bucket's load is the sum over its models of (requests in
+ *                   the trace x d_single) per device
+ *   partitions      per bucket and configuration c with cfg_devices[c] <=
+ *                   the bucket's devices: equal groups of configuration c and
+ *                   one last group with the remaining devices, whose
+ *                   configuration is the one of that device count with the
+ *                   deepest pipeline not deeper than c's (lowest index on
+ *                   ties; c is skipped if none exists or if the bucket would
+ *                   have more than AS_MAX_GROUPS groups)
+ *   selection       Alg. 1 places only the bucket's models, over the whole
+ *                   trace (other models' requests are never served there)
+ * trace, models, weight_mib as for as_greedy_placement.  Every Alg. 1 problem
+ * is solved once and all of them advance in lockstep (one launch per step).
+ * Synchronous on `stream`; allocates device memory for the candidate batches.
+ */
+int as_placement_search(const as_trace_t* trace, const as_models_t* models, const int64_t* weight_mib,
+                        const as_search_opts_t* opts, as_search_result_t* result, void* stream);
+
 /* Message of the last failed call on this thread ("" if none); valid until
  * the next call on this thread. */
 const char* as_last_error(void);

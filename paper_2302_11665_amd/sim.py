@@ -46,6 +46,31 @@ class as_job_t(ctypes.Structure):
                 ("slo_scale", ctypes.c_double)]
 
 
+AS_MAX_MODELS = 64
+AS_MAX_GROUPS = 64
+AS_MAX_BUCKETS = 8
+
+
+class as_search_opts_t(ctypes.Structure):
+    _fields_ = [("n_devices", ctypes.c_int32), ("device_unit", ctypes.c_int32),
+                ("device_mem_mib", ctypes.c_int64), ("cfg_devices", _P),
+                ("bucket_threshold", ctypes.c_double), ("balance_ratio", ctypes.c_double),
+                ("slo_scale", ctypes.c_double), ("max_buckets", ctypes.c_int32), ("beam", ctypes.c_int32)]
+
+
+class as_search_result_t(ctypes.Structure):
+    _fields_ = [("served", ctypes.c_int64), ("n_buckets", ctypes.c_int32),
+                ("n_bucket_configs", ctypes.c_int32), ("n_device_splits", ctypes.c_int32),
+                ("n_kept_splits", ctypes.c_int32), ("n_problems", ctypes.c_int32),
+                ("model_bucket", ctypes.c_int32 * AS_MAX_MODELS),
+                ("bucket_devices", ctypes.c_int32 * AS_MAX_BUCKETS),
+                ("bucket_cfg", ctypes.c_int32 * AS_MAX_BUCKETS),
+                ("bucket_groups", ctypes.c_int32 * AS_MAX_BUCKETS),
+                ("bucket_group_cfg", (ctypes.c_int32 * AS_MAX_GROUPS) * AS_MAX_BUCKETS),
+                ("bucket_served", ctypes.c_int64 * AS_MAX_BUCKETS),
+                ("bucket_mask", (ctypes.c_uint64 * AS_MAX_MODELS) * AS_MAX_BUCKETS)]
+
+
 AS_JOB_DTYPE = np.dtype([("placement", np.int32), ("segment", np.int32), ("slo_scale", np.float64)])
 assert AS_JOB_DTYPE.itemsize == ctypes.sizeof(as_job_t) == 16
 
@@ -93,6 +118,10 @@ def lib():
                                         ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, _P, _P, _P,
                                         _P, _P]
         L.as_simulate_stats.restype = ctypes.c_int
+        L.as_placement_search.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t), _P,
+                                          ctypes.POINTER(as_search_opts_t), ctypes.POINTER(as_search_result_t),
+                                          _P]
+        L.as_placement_search.restype = ctypes.c_int
         L.as_last_error.argtypes = []
         L.as_last_error.restype = ctypes.c_char_p
         L.as_version.argtypes = []
@@ -302,3 +331,34 @@ def as_partition_search(t, model, d_single, cfg_stages, stage_lat, weight_mib, p
     _check(rc)
     return {"best_partition": int(bp[0]), "best_mask": best, "best_served": int(bs[0]),
             "part_served": ps.tolist()}
+
+
+def as_placement_search(t, model, d_single, cfg_stages, stage_lat, weight_mib, cfg_devices, n_devices,
+                        device_unit, device_mem_mib, bucket_threshold, balance_ratio, max_buckets, beam,
+                        slo_scale, stream=None):
+    """Marshal to as_placement_search (Alg. 2).  Returns dict(served, buckets=[dict(models,
+    devices, cfg, group_cfg, mask, served)], n_bucket_configs, n_device_splits,
+    n_kept_splits, n_problems)."""
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    M = md.n_models
+    w = np.ascontiguousarray(weight_mib, dtype=np.int64)
+    cd = np.ascontiguousarray(cfg_devices, dtype=np.int32)
+    o = as_search_opts_t(int(n_devices), int(device_unit), int(device_mem_mib), cd.ctypes.data,
+                         float(bucket_threshold), float(balance_ratio), float(slo_scale), int(max_buckets),
+                         int(beam))
+    r = as_search_result_t()
+    rc = lib().as_placement_search(ctypes.byref(tr), ctypes.byref(md), w.ctypes.data, ctypes.byref(o),
+                                   ctypes.byref(r), _stream(stream))
+    _check(rc)
+    buckets = []
+    for b in range(r.n_buckets):
+        G = r.bucket_groups[b]
+        buckets.append({"models": [m for m in range(M) if r.model_bucket[m] == b],
+                        "devices": int(r.bucket_devices[b]), "cfg": int(r.bucket_cfg[b]),
+                        "group_cfg": np.array([r.bucket_group_cfg[b][g] for g in range(G)], np.int32),
+                        "mask": np.array([r.bucket_mask[b][m] for m in range(M)], np.uint64),
+                        "served": int(r.bucket_served[b])})
+    return {"served": int(r.served), "buckets": buckets, "n_bucket_configs": int(r.n_bucket_configs),
+            "n_device_splits": int(r.n_device_splits), "n_kept_splits": int(r.n_kept_splits),
+            "n_problems": int(r.n_problems)}
