@@ -284,6 +284,8 @@ typedef struct {
   int32_t n_device_splits;        /* device splits enumerated                          */
   int32_t n_kept_splits;          /* splits kept by the balance rule                   */
   int32_t n_problems;             /* Alg. 1 problems solved (bucket x devices x config) */
+  int64_t launches;               /* batched simulator launches of the search          */
+  int64_t jobs_simulated;         /* simulations run (each over the whole trace)       */
   int32_t model_bucket[AS_MAX_MODELS];                 /* bucket of each model       */
   int32_t bucket_devices[AS_MAX_BUCKETS];              /* devices of each bucket     */
   int32_t bucket_cfg[AS_MAX_BUCKETS];                  /* configuration of its equal

@@ -234,9 +234,11 @@ extern "C" int as_placement_search(const as_trace_t* trace, const as_models_t* m
     }
   }
   std::vector<Result> res;
+  SearchCount count;
   if (!probs.empty()) {
-    const int rc = o.beam == 0 ? fast_search(trace, models, weight_mib, o.slo_scale, probs, res, -1, s)
-                               : beam_search(trace, models, weight_mib, o.slo_scale, o.beam, probs, res, -1, s);
+    const int rc = o.beam == 0 ? fast_search(trace, models, weight_mib, o.slo_scale, probs, res, -1, s, &count)
+                               : beam_search(trace, models, weight_mib, o.slo_scale, o.beam, probs, res, -1, s,
+                                             &count);
     if (rc != AS_OK) return rc;
   }
   // each subproblem keeps its strictly best option (none: serves nothing)
@@ -268,6 +270,8 @@ extern "C" int as_placement_search(const as_trace_t* trace, const as_models_t* m
   result->n_device_splits = n_splits;
   result->n_kept_splits = (int32_t)kept.size();
   result->n_problems = (int32_t)probs.size();
+  result->launches = count.launches;
+  result->jobs_simulated = count.jobs;
   result->served = best;
   if (best_k >= 0) {
     const std::vector<int>& st = cuts[kept[best_k].first];

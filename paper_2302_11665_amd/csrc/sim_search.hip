@@ -25,9 +25,9 @@ namespace {
 
 // Candidate placements of one step: row p is base row cand[4p] with model
 // cand[4p+1] added to group cand[4p+2], in the group layout of search
-// cand[4p+3] (its row of cfg_tab).
+// cand[4p+3] (its row of cfg_tab, Gtab entries); rows have G groups.
 __global__ void expand_candidates(const uint64_t* __restrict__ base, const int32_t* __restrict__ cand,
-                                  const int32_t* __restrict__ cfg_tab, int P, int M, int G,
+                                  const int32_t* __restrict__ cfg_tab, int Gtab, int P, int M, int G,
                                   uint64_t* __restrict__ masks, int32_t* __restrict__ gcfg) {
   const int64_t nm = (int64_t)P * M, ng = (int64_t)P * G;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -39,10 +39,34 @@ __global__ void expand_candidates(const uint64_t* __restrict__ base, const int32
     } else {
       const int64_t k = i - nm;
       const int p = (int)(k / G), g = (int)(k % G);
-      gcfg[k] = cfg_tab[(int64_t)cand[4 * (int64_t)p + 3] * G + g];
+      gcfg[k] = g < Gtab ? cfg_tab[(int64_t)cand[4 * (int64_t)p + 3] * Gtab + g] : -1;
     }
   }
 }
+
+// Side streams and events of one search call (default priority), created on
+// first use and destroyed with the call.
+struct StreamPool {
+  std::vector<hipStream_t> st;
+  std::vector<hipEvent_t> ev;
+  hipError_t get(size_t k) {
+    while (st.size() <= k) {
+      hipStream_t x = nullptr;
+      hipEvent_t y = nullptr;
+      hipError_t e = hipStreamCreateWithFlags(&x, hipStreamNonBlocking);
+      if (e != hipSuccess) return e;
+      st.push_back(x);
+      e = hipEventCreateWithFlags(&y, hipEventDisableTiming);
+      if (e != hipSuccess) return e;
+      ev.push_back(y);
+    }
+    return hipSuccess;
+  }
+  ~StreamPool() {
+    for (hipStream_t x : st) hipStreamDestroy(x);
+    for (hipEvent_t y : ev) hipEventDestroy(y);
+  }
+};
 
 // Requests of each model in the trace (the fast heuristic's unserved counts
 // are these minus the served ones).
@@ -131,7 +155,7 @@ int check_search_common(const as_trace_t* trace, const as_models_t* models, cons
 // Alg. 1 with beam size `beam` on every problem, in lockstep.
 int beam_search(const as_trace_t* trace, const as_models_t* models, const int64_t* w, double slo_scale,
                 int beam, const std::vector<Problem>& probs, std::vector<Result>& res, int max_steps,
-                hipStream_t s) {
+                hipStream_t s, SearchCount* count) {
   if (beam < 1) return fail(AS_E_INVALID_ARG, "search: beam=%d < 1", beam);
   KArgs a;
   int smax = 1;
@@ -164,6 +188,23 @@ int beam_search(const as_trace_t* trace, const as_models_t* models, const int64_
   a.n = trace->n;
   a.slo_scale = static_cast<const double*>(d.p[1]);
   a.K = 1;
+  // kernel shape of each search: lanes per job (its group count rounded up
+  // to a power of two) and padded stage count (its deepest configuration)
+  std::vector<int> shape_of(R), shape_w, shape_s;
+  for (int r = 0; r < R; ++r) {
+    int sm = 1;
+    for (int g = 0; g < probs[r].G; ++g)
+      if (probs[r].cfg[g] >= 0) sm = std::max(sm, models->cfg_stages[probs[r].cfg[g]]);
+    const int wr = pow2ceil(probs[r].G), sr = pow2ceil(sm);
+    int k = 0;
+    while (k < (int)shape_w.size() && !(shape_w[k] == wr && shape_s[k] == sr)) ++k;
+    if (k == (int)shape_w.size()) {
+      shape_w.push_back(wr);
+      shape_s.push_back(sr);
+    }
+    shape_of[r] = k;
+  }
+  StreamPool pool;
 
   // candidate c of a step: (base row, model, group, search), and the new
   // selection it makes (kept on the host for dedup and the next beam)
@@ -207,35 +248,86 @@ int beam_search(const as_trace_t* trace, const as_models_t* models, const int64_
     first[R] = (int)news.size();
     const int P = (int)news.size();
     if (P == 0) break;
+    // one launch per kernel shape (lanes per job, padded stages), the shapes'
+    // launches running side by side on their own streams: a search's jobs are
+    // laid out for its own group count and pipeline depth, not the widest
+    std::vector<int> order(P);
+    for (int i = 0; i < P; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+      return shape_of[cand[4 * (size_t)x + 3]] < shape_of[cand[4 * (size_t)y + 3]];
+    });
+    std::vector<int32_t> cand_sorted((size_t)P * 4);
+    for (int i = 0; i < P; ++i)
+      for (int k = 0; k < 4; ++k) cand_sorted[4 * (size_t)i + k] = cand[4 * (size_t)order[i] + k];
+    struct Launch {
+      int shape, begin, end;
+      size_t gofs;
+    };
+    std::vector<Launch> launches;
+    size_t gtotal = 0;
+    for (int i = 0; i < P;) {
+      const int sh = shape_of[cand_sorted[4 * (size_t)i + 3]];
+      int j = i;
+      while (j < P && shape_of[cand_sorted[4 * (size_t)j + 3]] == sh) ++j;
+      launches.push_back({sh, i, j, gtotal});
+      gtotal += (size_t)(j - i) * shape_w[sh];
+      i = j;
+    }
     e = d.need(2, bases.size() * 8);
-    if (e == hipSuccess) e = d.need(3, cand.size() * 4);
+    if (e == hipSuccess) e = d.need(3, cand_sorted.size() * 4);
     if (e == hipSuccess) e = d.need(4, (size_t)P * M * 8);
-    if (e == hipSuccess) e = d.need(5, (size_t)P * G * 4);
+    if (e == hipSuccess) e = d.need(5, gtotal * 4);
     if (e == hipSuccess) e = d.need(6, (size_t)P * 8);
     if (e != hipSuccess) return fail(AS_E_NOMEM, "search: device allocation failed: %s", hipGetErrorString(e));
     e = hipMemcpyAsync(d.p[2], bases.data(), bases.size() * 8, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(d.p[3], cand.data(), cand.size() * 4, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) {
-      const int64_t work = (int64_t)P * (M + G);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(d.p[3], cand_sorted.data(), cand_sorted.size() * 4, hipMemcpyHostToDevice, s);
+    for (const Launch& L : launches) {
+      if (e != hipSuccess) break;
+      const int Pc = L.end - L.begin, Gc = shape_w[L.shape];
+      const int64_t work = (int64_t)Pc * (M + Gc);
       const int blocks = (int)std::min<int64_t>((work + 255) / 256, 4096);
       hipLaunchKernelGGL(expand_candidates, dim3(blocks), dim3(256), 0, s,
-                         static_cast<const uint64_t*>(d.p[2]), static_cast<const int32_t*>(d.p[3]),
-                         static_cast<const int32_t*>(d.p[0]), P, M, G, static_cast<uint64_t*>(d.p[4]),
-                         static_cast<int32_t*>(d.p[5]));
+                         static_cast<const uint64_t*>(d.p[2]),
+                         static_cast<const int32_t*>(d.p[3]) + 4 * (size_t)L.begin,
+                         static_cast<const int32_t*>(d.p[0]), G, Pc, M, Gc,
+                         static_cast<uint64_t*>(d.p[4]) + (size_t)L.begin * M,
+                         static_cast<int32_t*>(d.p[5]) + L.gofs);
       e = hipGetLastError();
     }
+    if (e == hipSuccess) e = pool.get(launches.size());
+    // the last event of the pool marks the expanded inputs on the caller's stream
+    if (e == hipSuccess) e = hipEventRecord(pool.ev[launches.size()], s);
     if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
-    a.group_cfg = static_cast<const int32_t*>(d.p[5]);
-    a.host_mask = static_cast<const uint64_t*>(d.p[4]);
-    a.out_served = static_cast<int64_t*>(d.p[6]);
-    a.P = P;
-    a.J = P;
-    rc = run_shared_trace(a, G, smax, s);
-    if (rc != AS_OK) return rc;
-    served.resize(P);
-    e = hipMemcpyAsync(served.data(), d.p[6], (size_t)P * 8, hipMemcpyDeviceToHost, s);
+    for (size_t k = 0; k < launches.size(); ++k) {
+      const Launch& L = launches[k];
+      hipStream_t sk = launches.size() == 1 ? s : pool.st[k];
+      if (sk != s && (e = hipStreamWaitEvent(sk, pool.ev[launches.size()], 0)) != hipSuccess)
+        return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+      KArgs ak = a;
+      ak.group_cfg = static_cast<const int32_t*>(d.p[5]) + L.gofs;
+      ak.host_mask = static_cast<const uint64_t*>(d.p[4]) + (size_t)L.begin * M;
+      ak.out_served = static_cast<int64_t*>(d.p[6]) + L.begin;
+      ak.P = L.end - L.begin;
+      ak.J = ak.P;
+      ak.G = shape_w[L.shape];
+      rc = run_shared_trace(ak, ak.G, shape_s[L.shape], sk);
+      if (rc != AS_OK) return rc;
+      if (sk != s) {
+        if ((e = hipEventRecord(pool.ev[k], sk)) != hipSuccess || (e = hipStreamWaitEvent(s, pool.ev[k], 0)) != hipSuccess)
+          return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+      }
+      if (count) {
+        count->launches += 1;
+        count->jobs += ak.P;
+      }
+    }
+    std::vector<int64_t> served_sorted(P);
+    e = hipMemcpyAsync(served_sorted.data(), d.p[6], (size_t)P * 8, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+    served.assign(P, 0);
+    for (int i = 0; i < P; ++i) served[order[i]] = served_sorted[i];
     for (int r = 0; r < R; ++r) {
       if (first[r] == first[r + 1]) continue;
       // top-k by served count, the earlier candidate first on ties
@@ -268,7 +360,7 @@ int beam_search(const as_trace_t* trace, const as_models_t* models, const int64_
 // most unserved requests on its available group with the least busy time.
 int fast_search(const as_trace_t* trace, const as_models_t* models, const int64_t* w, double slo_scale,
                 const std::vector<Problem>& probs, std::vector<Result>& res, int max_steps,
-                hipStream_t s) {
+                hipStream_t s, SearchCount* count) {
   KArgs a;
   int smax = 1;
   int rc = check_search_common(trace, models, w, slo_scale, probs, a, smax);
@@ -333,6 +425,10 @@ int fast_search(const as_trace_t* trace, const as_models_t* models, const int64_
                            static_cast<int64_t*>(d.p[4]), nullptr, static_cast<int64_t*>(d.p[5]),
                            static_cast<double*>(d.p[6]), s);
     if (rc != AS_OK) return rc;
+    if (count) {
+      count->launches += 1;
+      count->jobs += P;
+    }
     served.resize(P);
     ms.resize((size_t)P * M);
     busy.resize((size_t)P * G);

@@ -31,15 +31,22 @@ struct Result {
   std::vector<int64_t> step_served;
 };
 
+// Work done by a search call: batched launches and jobs (each job simulates
+// the whole trace once).
+struct SearchCount {
+  int64_t launches = 0;
+  int64_t jobs = 0;
+};
+
 // Alg. 1 with beam size `beam` on every problem; all candidates of all
 // active problems of a step are one batched launch.  max_steps < 0: no limit.
 int beam_search(const as_trace_t* trace, const as_models_t* models, const int64_t* weight_mib,
                 double slo_scale, int beam, const std::vector<Problem>& probs, std::vector<Result>& res,
-                int max_steps, hipStream_t s);
+                int max_steps, hipStream_t s, SearchCount* count = nullptr);
 
 // The fast heuristic on every problem; one job per active problem per step.
 int fast_search(const as_trace_t* trace, const as_models_t* models, const int64_t* weight_mib,
                 double slo_scale, const std::vector<Problem>& probs, std::vector<Result>& res,
-                int max_steps, hipStream_t s);
+                int max_steps, hipStream_t s, SearchCount* count = nullptr);
 
 }  // namespace as_host

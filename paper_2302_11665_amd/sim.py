@@ -62,6 +62,7 @@ class as_search_result_t(ctypes.Structure):
     _fields_ = [("served", ctypes.c_int64), ("n_buckets", ctypes.c_int32),
                 ("n_bucket_configs", ctypes.c_int32), ("n_device_splits", ctypes.c_int32),
                 ("n_kept_splits", ctypes.c_int32), ("n_problems", ctypes.c_int32),
+                ("launches", ctypes.c_int64), ("jobs_simulated", ctypes.c_int64),
                 ("model_bucket", ctypes.c_int32 * AS_MAX_MODELS),
                 ("bucket_devices", ctypes.c_int32 * AS_MAX_BUCKETS),
                 ("bucket_cfg", ctypes.c_int32 * AS_MAX_BUCKETS),
@@ -361,4 +362,5 @@ def as_placement_search(t, model, d_single, cfg_stages, stage_lat, weight_mib, c
                         "served": int(r.bucket_served[b])})
     return {"served": int(r.served), "buckets": buckets, "n_bucket_configs": int(r.n_bucket_configs),
             "n_device_splits": int(r.n_device_splits), "n_kept_splits": int(r.n_kept_splits),
-            "n_problems": int(r.n_problems)}
+            "n_problems": int(r.n_problems), "launches": int(r.launches),
+            "jobs_simulated": int(r.jobs_simulated)}
