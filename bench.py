@@ -18,7 +18,10 @@ groups) over a 16 x 16 x 16 grid of rate scale, CV and SLO scale, every grid
 point with its own 10-minute trace (4096 segments, about 4.4e8 requests) --
 timed the same way, with its HBM roofline (each segment is read once).
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep]
+And, as "search": wall time and simulated events of two placement searches
+(reduced and full Alg. 2) on the 32-model / 64-device workload.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep] [--no-search]
 """
 import argparse
 import json
@@ -43,15 +46,15 @@ HBM_PEAK = 8.0e12
 # change, traffic is reported as null until it is measured again.
 KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd/csrc/sim_kernel.hpp",
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
-                  "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_internal.hpp"]
+                  "paper_2302_11665_amd/csrc/sim_shared.hpp"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "e250e1b629735ddc321826e744c878ee5fb5e8c938f0a2692de1bc42bc96e85b",
+    "sources_sha256": "10b11393c0c9cbea45719d5db0ee9d5202cb321622bcf82168aeb0399f32c2d2",
     "kernel": "shared_kernel<16, 4, true>",
     "fetch_kib": 327576.3125, "write_kib": 450111.0,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "e250e1b629735ddc321826e744c878ee5fb5e8c938f0a2692de1bc42bc96e85b",
+    "sources_sha256": "10b11393c0c9cbea45719d5db0ee9d5202cb321622bcf82168aeb0399f32c2d2",
     "kernel": "seg_kernel<1>",
     "fetch_kib": 2595204.0, "write_kib": 13847.75,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
@@ -167,6 +170,49 @@ def bench_sweep(args, np, torch, api, problems):
             "trace_gen_s": round(gen_s, 3), "upload_s": round(up_s, 3)}
 
 
+def bench_search(args, np, torch, sim, problems):
+    """Placement searches on the 32-model / 64-device workload (Gamma 4 req/s
+    per model, CV 2, 20 minutes, SLO scale 5): the reduced Alg. 2 (Alg. 1 with
+    beam 1 on each of the 10 uniform partitions), whose oracle run is stored
+    with its wall time, and the full Alg. 2 with up to 3 model buckets."""
+    with open(os.path.join(ROOT, "tests", "golden", "c3_greedy_oracle.json")) as f:
+        fx = json.load(f)
+    gp = problems.c3_greedy()
+    N = len(gp.t)
+    d = sim.to_device
+    t, m, ds, L = d(gp.t), d(gp.model), d(gp.d_single), d(gp.stage_lat)
+    cd = (gp.cfg_stages * gp.cfg_k).astype(np.int32)
+    out = {"workload": "32 models (d ~ U[0.05,0.8] s, w ~ U[1,13] GB), 64 x 32 GB devices, Gamma 4 req/s/model "
+                       "CV 2, 1200 s, SLO scale 5; configurations (S,k) with S*k in {1,2,4,8}",
+           "requests": N}
+    runs = [("alg2_reduced", dict(max_buckets=1, bucket_threshold=10.0, balance_ratio=float("inf"),
+                                  device_unit=64, beam=1)),
+            ("alg2_full", dict(max_buckets=3, bucket_threshold=0.4, balance_ratio=2.0, device_unit=16, beam=1))]
+    for name, kw in runs:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = sim.as_placement_search(t, m, ds, gp.cfg_stages, L, gp.weight_mib, cd, 64, kw["device_unit"],
+                                    gp.meta["device_mem_mib"], kw["bucket_threshold"], kw["balance_ratio"],
+                                    kw["max_buckets"], kw["beam"], gp.slo_scale)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ev = r["jobs_simulated"] * N
+        opts = {k: ("inf" if isinstance(v, float) and v == float("inf") else v) for k, v in kw.items()}
+        res = {"options": opts, "wall_s": round(wall, 3), "launches": r["launches"], "jobs": r["jobs_simulated"],
+               "events": ev, "events_per_s": round(ev / wall, 1), "served": r["served"],
+               "problems": r["n_problems"], "kept_splits": r["n_kept_splits"],
+               "buckets": [{"models": b["models"], "devices": b["devices"], "cfg": b["cfg"], "served": b["served"]}
+                           for b in r["buckets"]]}
+        if name == "alg2_reduced":
+            res["oracle_served"] = fx["best_served"]
+            res["oracle_wall_s"] = round(fx["seconds"], 1)
+            res["oracle_note"] = "the same search on the CPU oracle, 8 threads (stored with its result)"
+            res["parity"] = r["served"] == fx["best_served"]
+        log(f"search {name}: {wall:.2f}s, {r['launches']} launches, {r['jobs_simulated']} jobs, served {r['served']}")
+        out[name] = res
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +223,7 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=192, help="jobs timed on the CPU oracle")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true", help="skip the SLO-curve sweep workload")
+    ap.add_argument("--no-search", action="store_true", help="skip the placement-search timings")
     ap.add_argument("--sweep-only", action="store_true",
                     help="time only the SLO-curve sweep (prints its object alone)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
@@ -293,6 +340,8 @@ def main():
         del dp
         torch.cuda.empty_cache()
         out["sweep"] = bench_sweep(args, np, torch, api, problems)
+    if not args.no_search:
+        out["search"] = bench_search(args, np, torch, sim, problems)
     print(json.dumps(out), flush=True)
 
 
