@@ -61,6 +61,11 @@ class OracleLib:
             g.argtypes = f.argtypes + [P, P]
             g.restype = ctypes.c_int
         self._fn_stats = g
+        h = getattr(self._lib, "oracle_simulate_job_batched", None)
+        if h is not None:
+            h.argtypes = f.argtypes[:13] + [ctypes.c_int32, ctypes.c_double, P, P, P, P]
+            h.restype = ctypes.c_int
+        self._fn_batched = h
 
     def simulate_job(self, t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
                      slo_scale, want_finish=False):
@@ -118,6 +123,33 @@ class OracleLib:
         if rc != 0:
             raise ValueError(f"oracle_simulate_job_stats rejected its arguments (rc={rc})")
         return int(served[0]), (int(digest[0]), int(digest[1])), ms, busy
+
+    def simulate_job_batched(self, t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
+                             slo_scale, max_batch, beta):
+        """Dynamic batching (Sec. 6.5).  Returns (served, (h, fin_sum), finish
+        float64[n], batch int32[n]) -- h is the order-free digest of the batched
+        variant (sum of mix(i) over served requests)."""
+        t = np.ascontiguousarray(t, dtype=np.float64)
+        model = np.ascontiguousarray(model, dtype=np.int32)
+        d_single = np.ascontiguousarray(d_single, dtype=np.float64)
+        cfg_stages = np.ascontiguousarray(cfg_stages, dtype=np.int32)
+        stage_lat = np.ascontiguousarray(stage_lat, dtype=np.float64)
+        group_cfg = np.ascontiguousarray(group_cfg, dtype=np.int32)
+        host_mask = np.ascontiguousarray(host_mask, dtype=np.uint64)
+        n = t.shape[0]
+        M, C, S = stage_lat.shape
+        served = np.zeros(1, dtype=np.int64)
+        digest = np.zeros(2, dtype=np.uint64)
+        finish = np.empty(n, dtype=np.float64)
+        batch = np.empty(n, dtype=np.int32)
+        rc = self._fn_batched(n, t.ctypes.data, model.ctypes.data, M, d_single.ctypes.data, C,
+                              cfg_stages.ctypes.data, S, stage_lat.ctypes.data, group_cfg.shape[0],
+                              group_cfg.ctypes.data, host_mask.ctypes.data, float(slo_scale), int(max_batch),
+                              float(beta), served.ctypes.data, digest.ctypes.data, finish.ctypes.data,
+                              batch.ctypes.data)
+        if rc != 0:
+            raise ValueError(f"oracle_simulate_job_batched rejected its arguments (rc={rc})")
+        return int(served[0]), (int(digest[0]), int(digest[1])), finish, batch
 
     def simulate_placements(self, t, model, d_single, cfg_stages, stage_lat, group_cfg,
                             host_mask, slo_scale, finish_jobs=(), threads=None):

@@ -118,3 +118,108 @@ def simulate(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, sl
     if return_groups:
         return served, finish, chosen
     return served, finish
+
+
+def _mix64(z):
+    M64 = (1 << 64) - 1
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & M64
+    return z ^ (z >> 31)
+
+
+def simulate_batched(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
+                     max_batch, beta):
+    """Dynamic batching (Sec. 6.5) as an event-driven simulation: a global clock
+    walks through arrival events and group-idle events; every group keeps the
+    list of batches it ran, and its stage timelines come from replaying them
+    through explicit stage servers (a batch is one unit whose stage latencies
+    are the model's times (1 + beta (b - 1))).  Rules as in the C oracle's
+    batched simulation.  Returns (served, finish[n], batch[n], digest)."""
+    t = [float(x) for x in t]
+    model = [int(x) for x in model]
+    n, G = len(t), len(group_cfg)
+    ran = {g: ([], []) for g in range(G)}  # g -> (batch start times, latency rows)
+    queue = {m: [] for m in range(len(d_single))}
+    finish = np.array([-2.0 if int(host_mask[m]) == 0 else -1.0 for m in model], dtype=np.float64)
+    batch = np.zeros(n, dtype=np.int32)
+
+    def rows(g, m, b):
+        c = int(group_cfg[g])
+        fac = 1.0 + float(beta) * float(b - 1)
+        return [float(stage_lat[m][c][s]) * fac for s in range(int(cfg_stages[c]))]
+
+    def free0(g):
+        starts, lat = ran[g]
+        dep = _replay(starts, lat)
+        return dep[-1][0] if dep else 0.0
+
+    def run(g, m, b, x):
+        starts, lat = ran[g]
+        dep = _replay(starts + [x], lat + [rows(g, m, b)])
+        return dep[-1][-1]
+
+    def commit(g, m, b, x):
+        ran[g][0].append(x)
+        ran[g][1].append(rows(g, m, b))
+
+    def hosts(m, g):
+        return (int(host_mask[m]) >> g) & 1
+
+    i = 0
+    while True:
+        # next idle event among groups with queued work for a hosted model
+        ev = None
+        for g in range(G):
+            if int(group_cfg[g]) < 0 or not any(queue[m] and hosts(m, g) for m in queue):
+                continue
+            x = free0(g)
+            if ev is None or x < ev[0]:
+                ev = (x, g)
+        if ev is not None and (i >= n or ev[0] <= t[i]):
+            tau, g = ev
+            while True:
+                cands = [m for m in queue if queue[m] and hosts(m, g)]
+                if not cands:
+                    break
+                m = min(cands, key=lambda mm: queue[mm][0])
+                head = queue[m][0]
+                dl = t[head] + float(slo_scale) * float(d_single[m])
+                best = 0
+                for b in range(1, min(max_batch, len(queue[m])) + 1):
+                    if run(g, m, b, tau) > dl:
+                        break
+                    best = b
+                if best == 0:
+                    queue[m].pop(0)
+                    continue
+                fin = run(g, m, best, tau)
+                commit(g, m, best, tau)
+                for r in queue[m][:best]:
+                    finish[r] = fin
+                    batch[r] = best
+                del queue[m][:best]
+                break
+            continue
+        if i >= n:
+            break
+        m = model[i]
+        if int(host_mask[m]) != 0:
+            avail = [(free0(g), g) for g in range(G) if hosts(m, g) and free0(g) <= t[i]]
+            if avail:
+                _, g = min(avail)
+                fin = run(g, m, 1, t[i])
+                if not fin > t[i] + float(slo_scale) * float(d_single[m]):
+                    commit(g, m, 1, t[i])
+                    finish[i] = fin
+                    batch[i] = 1
+            else:
+                queue[m].append(i)
+        i += 1
+    served = int((batch > 0).sum())
+    h = 0
+    fs = 0
+    for r in range(n):
+        if batch[r] > 0:
+            h = (h + _mix64(r)) & ((1 << 64) - 1)
+            fs = (fs + int(np.float64(finish[r]).view(np.uint64))) & ((1 << 64) - 1)
+    return served, finish, batch, (h, fs)

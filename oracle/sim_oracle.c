@@ -197,3 +197,203 @@ int oracle_simulate_job(int64_t n, const double* t, const int32_t* model, int32_
                                    stage_lat, n_groups, group_cfg, host_mask, slo_scale, served_out,
                                    digest_out, finish_out, NULL, NULL);
 }
+
+/*
+ * Dynamic batching (Sec. 6.5).  The paper's batching strategy: a request
+ * that arrives while a device group hosting its model is available runs at
+ * once; otherwise it waits in a per-model queue; a group that becomes idle
+ * picks a model it hosts and runs as many of that model's queued requests
+ * as possible in one batch while the SLO holds.  A batch's execution latency
+ * grows linearly with its size.
+ *
+ * Readings (each one also stated in the design notes):
+ *   - a group is available, and becomes idle, when its stage 0 is free: at
+ *     time x it is available iff F[g][0] <= x; among available hosting
+ *     groups the one with the smallest F[g][0] runs an arriving request
+ *     (lowest index on ties);
+ *   - stage latencies of a batch of b requests of model m on configuration c:
+ *     L[m][c][s] * (1 + beta * (b - 1)), the factor rounded once, then the
+ *     product (beta >= 0; beta = 1: no throughput gain from batching);
+ *   - a batch starting at x runs through the group's stages like one request:
+ *     f_{-1} = x, f_s = max(f_{s-1}, F[g][s]) + lat_s; every request of the
+ *     batch finishes at f_{S-1}; F[g][s] := f_s;
+ *   - an arriving request that runs at once is served iff its finish is
+ *     within its deadline t + slo_m; otherwise it is dropped;
+ *   - a group becomes idle at tau = F[g][0]; if a model it hosts has queued
+ *     requests it starts a batch at tau: the model whose queue head arrived
+ *     first (lowest trace index); the batch takes the largest b <=
+ *     min(max_batch, queue length) whose finish is within the head's deadline
+ *     (the tightest of the model's queue, which is FIFO); if even b = 1 misses
+ *     it, the head is dropped and the choice is made again; with no queued
+ *     work the group stays idle;
+ *   - before an arrival at t, every idle event at tau <= t is handled, in
+ *     order of tau, lowest group first on ties; after the last arrival the
+ *     remaining idle events are handled until no queued work remains.
+ * Outputs as for the unbatched simulation, except the digest, which cannot
+ * fold accept words in trace order because queued requests are decided
+ * later: h = sum mod 2^64 over served requests i of mix(i), where mix is the
+ * SplitMix64 finaliser of i; fin_sum as before.  batch_out[i] (may be NULL):
+ * size of the batch request i ran in, 0 if not served.
+ */
+static uint64_t oracle_mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+typedef struct {
+  int64_t* idx; /* queued trace indices, FIFO from head */
+  int64_t head, tail, cap;
+} oracle_queue;
+
+static int oracle_queue_push(oracle_queue* q, int64_t i) {
+  if (q->tail == q->cap) {
+    int64_t cap = q->cap ? 2 * q->cap : 16;
+    int64_t* p = (int64_t*)realloc(q->idx, (size_t)cap * sizeof(int64_t));
+    if (!p) return ORACLE_E_NOMEM;
+    q->idx = p;
+    q->cap = cap;
+  }
+  q->idx[q->tail++] = i;
+  return ORACLE_OK;
+}
+
+int oracle_simulate_job_batched(int64_t n, const double* t, const int32_t* model, int32_t n_models,
+                                const double* d_single, int32_t n_configs, const int32_t* cfg_stages,
+                                int32_t max_stages, const double* stage_lat, int32_t n_groups,
+                                const int32_t* group_cfg, const uint64_t* host_mask, double slo_scale,
+                                int32_t max_batch, double beta, int64_t* served_out, uint64_t* digest_out,
+                                double* finish_out, int32_t* batch_out) {
+  if (n < 0 || n_models <= 0 || n_configs <= 0 || max_stages <= 0 || n_groups <= 0 || n_groups > 64 ||
+      max_batch < 1 || !(beta >= 0.0) || !served_out || !digest_out)
+    return ORACLE_E_ARG;
+  for (int32_t c = 0; c < n_configs; ++c)
+    if (cfg_stages[c] < 1 || cfg_stages[c] > max_stages) return ORACLE_E_ARG;
+  for (int32_t m = 0; m < n_models; ++m)
+    for (int32_t g = 0; g < 64; ++g)
+      if ((host_mask[m] >> g) & 1u)
+        if (g >= n_groups || group_cfg[g] < 0 || group_cfg[g] >= n_configs) return ORACLE_E_ARG;
+  for (int64_t i = 0; i < n; ++i)
+    if (model[i] < 0 || model[i] >= n_models) return ORACLE_E_ARG;
+
+  double* F = (double*)calloc((size_t)n_groups * (size_t)max_stages, sizeof(double));
+  double* slo = (double*)malloc((size_t)n_models * sizeof(double));
+  double* f = (double*)malloc((size_t)max_stages * sizeof(double));
+  oracle_queue* q = (oracle_queue*)calloc((size_t)n_models, sizeof(oracle_queue));
+  int rc = ORACLE_OK;
+  if (!F || !slo || !f || !q) {
+    rc = ORACLE_E_NOMEM;
+    goto done;
+  }
+  for (int32_t m = 0; m < n_models; ++m) slo[m] = slo_scale * d_single[m];
+  int64_t served = 0;
+  uint64_t h = 0, fin_sum = 0;
+  if (finish_out)
+    for (int64_t i = 0; i < n; ++i) finish_out[i] = (host_mask[model[i]] == 0) ? -2.0 : -1.0;
+  if (batch_out)
+    for (int64_t i = 0; i < n; ++i) batch_out[i] = 0;
+
+/* finish of a batch of b requests of model m started at x on group g, into f[] */
+#define ORACLE_BATCH_FINISH(g, m, b, x)                                                   \
+  do {                                                                                    \
+    const int32_t c_ = group_cfg[g];                                                      \
+    const double fac_ = 1.0 + beta * (double)((b) - 1);                                  \
+    double prev_ = (x);                                                                   \
+    for (int32_t s_ = 0; s_ < cfg_stages[c_]; ++s_) {                                     \
+      const double lat_ = stage_lat[((int64_t)(m) * n_configs + c_) * max_stages + s_] * fac_; \
+      f[s_] = oracle_max(prev_, F[(g) * max_stages + s_]) + lat_;                         \
+      prev_ = f[s_];                                                                      \
+    }                                                                                     \
+  } while (0)
+
+  for (int64_t i = 0; i <= n; ++i) {
+    /* idle events up to the next arrival (all of them after the last one) */
+    const double horizon = i < n ? t[i] : 0.0;
+    for (;;) {
+      int32_t gs = -1;
+      for (int32_t g = 0; g < n_groups; ++g) {
+        if (group_cfg[g] < 0) continue;
+        int work = 0;
+        for (int32_t m = 0; m < n_models && !work; ++m)
+          work = ((host_mask[m] >> g) & 1u) && q[m].head < q[m].tail;
+        if (!work) continue;
+        if (gs < 0 || F[g * max_stages] < F[gs * max_stages]) gs = g;
+      }
+      if (gs < 0) break;
+      const double tau = F[gs * max_stages];
+      if (i < n && !(tau <= horizon)) break;
+      /* the group starts a batch at tau, or drops expired heads until it can */
+      for (;;) {
+        int32_t mc = -1;
+        for (int32_t m = 0; m < n_models; ++m)
+          if (((host_mask[m] >> gs) & 1u) && q[m].head < q[m].tail &&
+              (mc < 0 || q[m].idx[q[m].head] < q[mc].idx[q[mc].head]))
+            mc = m;
+        if (mc < 0) break; /* nothing left for this group: it stays idle */
+        const int64_t hd = q[mc].idx[q[mc].head];
+        const double dl = t[hd] + slo[mc];
+        const int64_t avail = q[mc].tail - q[mc].head;
+        const int32_t bmax = avail < max_batch ? (int32_t)avail : max_batch;
+        int32_t b = 0;
+        for (int32_t bb = 1; bb <= bmax; ++bb) {
+          ORACLE_BATCH_FINISH(gs, mc, bb, tau);
+          if (f[cfg_stages[group_cfg[gs]] - 1] > dl) break;
+          b = bb;
+        }
+        if (b == 0) {
+          q[mc].head += 1; /* the head cannot meet its deadline: dropped */
+          continue;
+        }
+        ORACLE_BATCH_FINISH(gs, mc, b, tau);
+        const int32_t S = cfg_stages[group_cfg[gs]];
+        for (int32_t s = 0; s < S; ++s) F[gs * max_stages + s] = f[s];
+        const double fin = f[S - 1];
+        for (int32_t k = 0; k < b; ++k) {
+          const int64_t r = q[mc].idx[q[mc].head + k];
+          served += 1;
+          h += oracle_mix64((uint64_t)r);
+          fin_sum += bits_of(fin);
+          if (finish_out) finish_out[r] = fin;
+          if (batch_out) batch_out[r] = b;
+        }
+        q[mc].head += b;
+        break;
+      }
+    }
+    if (i == n) break;
+    /* the arrival */
+    const int32_t m = model[i];
+    const uint64_t mask = host_mask[m];
+    if (mask == 0) continue;
+    int32_t ga = -1;
+    for (int32_t g = 0; g < n_groups; ++g)
+      if (((mask >> g) & 1u) && F[g * max_stages] <= t[i] && (ga < 0 || F[g * max_stages] < F[ga * max_stages]))
+        ga = g;
+    if (ga >= 0) {
+      ORACLE_BATCH_FINISH(ga, m, 1, t[i]);
+      const int32_t S = cfg_stages[group_cfg[ga]];
+      if (!(f[S - 1] > t[i] + slo[m])) {
+        for (int32_t s = 0; s < S; ++s) F[ga * max_stages + s] = f[s];
+        served += 1;
+        h += oracle_mix64((uint64_t)i);
+        fin_sum += bits_of(f[S - 1]);
+        if (finish_out) finish_out[i] = f[S - 1];
+        if (batch_out) batch_out[i] = 1;
+      }
+    } else if ((rc = oracle_queue_push(&q[m], i)) != ORACLE_OK) {
+      goto done;
+    }
+  }
+#undef ORACLE_BATCH_FINISH
+  *served_out = served;
+  digest_out[0] = h;
+  digest_out[1] = fin_sum;
+done:
+  if (q)
+    for (int32_t m = 0; m < n_models; ++m) free(q[m].idx);
+  free(q);
+  free(F);
+  free(slo);
+  free(f);
+  return rc;
+}
