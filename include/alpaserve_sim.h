@@ -257,6 +257,57 @@ int as_simulate_stats(const as_trace_t* trace, const as_models_t* models,
                       int64_t* out_served, uint64_t* out_digest, int64_t* out_model_served,
                       double* out_group_busy, void* stream);
 
+/*
+ * Dynamic batching (Sec. 6.5).  The same jobs as as_simulate_placements (job
+ * j = p * K + k), simulated with the paper's batching strategy: a request
+ * that arrives while a group hosting its model is available runs at once,
+ * otherwise it waits in a per-model queue; a group that becomes idle picks a
+ * model it hosts and runs as many of its queued requests as possible in one
+ * batch while the SLO holds.  Exact rules:
+ *   - a group is available, and becomes idle, when its stage 0 is free: at
+ *     time x iff F[g][0] <= x.  An arriving request (time t, model m) runs on
+ *     the available hosting group with the smallest F[g][0] (lowest index on
+ *     ties) as a batch of one starting at t, and is served iff its finish is
+ *     <= t + scale * d_single[m]; otherwise it is dropped.  With no available
+ *     hosting group it joins the tail of m's queue;
+ *   - a batch of b requests of model m on group g with configuration c
+ *     starting at x: stage latencies lat_s = L[m][c][s] * (1 + beta*(b-1))
+ *     (the factor rounded once, then the product), f_{-1} = x, f_s =
+ *     max(f_{s-1}, F[g][s]) + lat_s; all b requests finish at f_{S-1}, and
+ *     F[g][s] := f_s;
+ *   - a group becomes idle at tau = F[g][0].  If models it hosts have queued
+ *     requests it starts a batch at tau: of the model whose queue head has
+ *     the lowest trace index, the largest b <= min(max_batch, queue length)
+ *     whose finish is <= the head's deadline (the tightest in that FIFO
+ *     queue).  If b = 1 misses it, the head is dropped and the choice is made
+ *     again.  With no queued work the group stays idle;
+ *   - before each arrival at t every idle event at tau <= t is handled, in
+ *     order of tau, lowest group first on ties; after the last arrival the
+ *     remaining ones are handled until no queued work remains.
+ *   beta            latency slope, finite, >= 0 (1: a batch of b takes b times
+ *                   as long as one request, as for GPUs a small batch saturates)
+ *   max_batch       >= 1
+ *   queue_cap       capacity of each model's queue per job, a power of two;
+ *                   the queues live in LDS (M * queue_cap * 4 bytes per job,
+ *                   AS_E_LIMITS if that and the tables exceed a workgroup's LDS);
+ *                   if a queue would overflow, the call returns AS_E_LIMITS
+ *                   and its results are incomplete
+ *   out_served[J]   served counts
+ *   out_digest[J][2] {h, fin_sum} or NULL, where h = sum mod 2^64 over served
+ *                   requests i of mix(i), mix the SplitMix64 finaliser
+ *                   (queued requests are decided out of trace order, so the
+ *                   accept-word fold of the other entry points does not apply)
+ *   finish_jobs, n_finish, out_finish as for as_simulate_placements (finish
+ *                   time of a served request, -1 dropped, -2 no hosting group)
+ * Synchronous on `stream` (it reads back the overflow flag); allocates 4
+ * bytes of device memory per call.  One job per wavefront, lanes = groups.
+ */
+int as_simulate_batched(const as_trace_t* trace, const as_models_t* models,
+                        const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
+                        int32_t max_batch, double beta, int32_t queue_cap, int64_t* out_served,
+                        uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
+                        double* out_finish, void* stream);
+
 #define AS_MAX_BUCKETS 8 /* model buckets of one placement (Alg. 2) */
 
 /* Options of as_placement_search (Alg. 2).  HOST struct. */

@@ -123,6 +123,10 @@ def lib():
                                           ctypes.POINTER(as_search_opts_t), ctypes.POINTER(as_search_result_t),
                                           _P]
         L.as_placement_search.restype = ctypes.c_int
+        L.as_simulate_batched.argtypes = [ctypes.POINTER(as_trace_t), ctypes.POINTER(as_models_t),
+                                          ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_double, ctypes.c_int32, _P, _P, _P, ctypes.c_int32, _P, _P]
+        L.as_simulate_batched.restype = ctypes.c_int
         L.as_last_error.argtypes = []
         L.as_last_error.restype = ctypes.c_char_p
         L.as_version.argtypes = []
@@ -364,3 +368,20 @@ def as_placement_search(t, model, d_single, cfg_stages, stage_lat, weight_mib, c
             "n_device_splits": int(r.n_device_splits), "n_kept_splits": int(r.n_kept_splits),
             "n_problems": int(r.n_problems), "launches": int(r.launches),
             "jobs_simulated": int(r.jobs_simulated)}
+
+
+def as_simulate_batched(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
+                        max_batch, beta, out_served, out_digest=None, finish_jobs=None, out_finish=None,
+                        queue_cap=1024, stream=None):
+    """Marshal to as_simulate_batched (dynamic batching, Sec. 6.5); device
+    tensors as for as_simulate_placements."""
+    tr = as_trace_t(int(t.shape[0]), _ptr(t), _ptr(model))
+    md, _keep = make_models(d_single, cfg_stages, stage_lat)
+    pl = make_placements(group_cfg, host_mask)
+    fj = None if finish_jobs is None else np.ascontiguousarray(finish_jobs, dtype=np.int32)
+    nf = 0 if fj is None else int(fj.shape[0])
+    rc = lib().as_simulate_batched(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl), _ptr(slo_scale),
+                                   int(slo_scale.shape[0]), int(max_batch), float(beta), int(queue_cap),
+                                   _ptr(out_served), _ptr(out_digest), _ptr(fj), nf, _ptr(out_finish),
+                                   _stream(stream))
+    _check(rc)

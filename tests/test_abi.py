@@ -157,3 +157,25 @@ def test_search_and_stats_argument_errors(L):
               None) == sim.AS_E_INVALID_ARG
     assert st(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(sim.as_placements_t(0, 4, None, None)), 0x50, 1,
               None, None, None, None, None) == sim.AS_OK
+
+
+def test_batched_argument_errors(L):
+    md, _k = _models(M=2)
+    tr = sim.as_trace_t(4, 0x10, 0x20)
+    pl = sim.as_placements_t(3, 4, 0x30, 0x40)
+    f = L.as_simulate_batched
+
+    def call(trace=tr, K=1, B=2, beta=1.0, qcap=64, served=0x60, placements=pl):
+        return f(ctypes.byref(trace) if trace is not None else None, ctypes.byref(md), ctypes.byref(placements),
+                 0x50, K, B, beta, qcap, served, None, None, 0, None, None)
+
+    assert call(trace=None) == sim.AS_E_INVALID_ARG
+    assert call(B=0) == sim.AS_E_INVALID_ARG
+    assert call(beta=-1.0) == sim.AS_E_INVALID_ARG
+    assert call(beta=float("nan")) == sim.AS_E_INVALID_ARG
+    assert call(qcap=48) == sim.AS_E_INVALID_ARG  # not a power of two
+    assert call(qcap=0) == sim.AS_E_INVALID_ARG
+    assert call(K=-1) == sim.AS_E_INVALID_ARG
+    assert call(served=None) == sim.AS_E_INVALID_ARG
+    assert call(qcap=1 << 20) == sim.AS_E_LIMITS  # queues do not fit in LDS
+    assert call(placements=sim.as_placements_t(0, 4, None, None)) == sim.AS_OK

@@ -1,0 +1,141 @@
+"""GPU parity of the dynamic-batching simulation (Sec. 6.5) against the
+oracle, bit-exact: served counts, the order-free digest and every
+per-request finish time, for 1 to 64 groups, 1 to 8 stages, several maximum
+batch sizes, latency slopes and SLO scales (0 and +inf included), ragged
+traces, and the batching experiment's workload shape (16 models on groups of
+4 devices, a bursty Gamma trace, batch sizes 1-8 at slope 1), plus a queue
+overflow that must be reported rather than ignored."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+from gpu_common import say  # noqa: E402
+
+import oracle  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+INF = float("inf")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2302_11665_amd import sim
+    return sim
+
+
+def _case(rng, G, Smax, M, n, P=4):
+    C = min(G, 5)
+    cfg_stages = rng.integers(1, Smax + 1, C).astype(np.int32)
+    cfg_stages[0] = Smax
+    L = rng.uniform(0.02, 0.5, (M, C, Smax))
+    gaps = rng.exponential(0.4 / max(G, 1), n)
+    gaps[rng.random(n) < 0.25] = 0.0
+    t = np.cumsum(gaps)
+    model = rng.integers(0, M, n).astype(np.int32)
+    d_single = L[:, 0, :].sum(axis=1) / rng.uniform(0.5, 1.5, M)
+    group_cfg = rng.integers(-1, C, (P, G)).astype(np.int32)
+    group_cfg[:, 0] = 0
+    host_mask = np.zeros((P, M), np.uint64)
+    for p in range(P):
+        for m in range(M):
+            bits = 0
+            for g in range(G):
+                if group_cfg[p, g] >= 0 and rng.random() < 0.4:
+                    bits |= 1 << g
+            host_mask[p, m] = np.uint64(bits)
+    return t, model, d_single, cfg_stages, L, group_cfg, host_mask
+
+
+def _run(dev, t, model, d, cs, L, gc, hm, scales, B, beta, fj, qcap=1024):
+    import torch
+    dd = dev.to_device
+    J = gc.shape[0] * len(scales)
+    served = torch.empty(J, dtype=torch.int64, device="cuda")
+    digest = torch.empty((J, 2), dtype=torch.int64, device="cuda")
+    fin = torch.empty((len(fj), len(t)), dtype=torch.float64, device="cuda") if len(fj) else None
+    dev.as_simulate_batched(dd(t), dd(model), dd(d), cs, dd(L), dd(gc), dd(hm), dd(np.asarray(scales, np.float64)),
+                            B, beta, served, digest, np.asarray(fj, np.int32) if len(fj) else None, fin,
+                            queue_cap=qcap)
+    return served.cpu().numpy(), dev.u64(digest), (fin.cpu().numpy() if fin is not None else None)
+
+
+def _check(lib, t, model, d, cs, L, gc, hm, scales, B, beta, served, digest, fin, fj):
+    K = len(scales)
+    rows = {int(j): f for f, j in enumerate(fj)}
+    for j in range(gc.shape[0] * K):
+        p, k = divmod(j, K)
+        s, dg, ofin, _ = lib.simulate_job_batched(t, model, d, cs, L, gc[p], hm[p], scales[k], B, beta)
+        assert int(served[j]) == s, (j, served[j], s)
+        assert tuple(int(x) for x in digest[j]) == dg, j
+        if j in rows:
+            g = fin[rows[j]]
+            if g.tobytes() != ofin.tobytes():
+                i = int(np.nonzero(g.view(np.uint64) != ofin.view(np.uint64))[0][0])
+                raise AssertionError((j, i, g[i], ofin[i]))
+
+
+@pytest.mark.parametrize("G,Smax,B,beta", [(1, 1, 1, 1.0), (1, 2, 4, 0.5), (3, 2, 2, 1.0), (4, 4, 8, 0.25),
+                                           (16, 1, 3, 0.0), (17, 3, 4, 0.75), (40, 8, 2, 0.5), (64, 2, 16, 1.0)])
+def test_batching_matches_oracle(dev, G, Smax, B, beta):
+    rng = np.random.default_rng(300 + G * 7 + Smax * 3 + B)
+    M = 6
+    n = 1500 + 13 * G
+    t, model, d, cs, L, gc, hm = _case(rng, G, Smax, M, n)
+    scales = [2.0, INF, 0.0, 5.0]
+    fj = [0, 5, 9, gc.shape[0] * len(scales) - 1]
+    say("batching", G, Smax, B, beta, n)
+    served, digest, fin = _run(dev, t, model, d, cs, L, gc, hm, scales, B, beta, fj)
+    _check(oracle.lib(), t, model, d, cs, L, gc, hm, scales, B, beta, served, digest, fin, fj)
+
+
+def test_batching_experiment_workload(dev):
+    """The batching experiment's shape: 16 models on 4 groups of 4 devices
+    (S=4), Gamma CV 3 at 4 req/s per model (the experiment used CV 4), maximum batch sizes 1, 2, 4, 8 at
+    slope 1 (a small batch saturates the device), SLO scales 1 to 10."""
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c2_greedy_step(duration=120.0)
+    rng = np.random.default_rng(9)
+    P = 12
+    gc = pb.group_cfg[:P]
+    hm = pb.host_mask[:P].copy()
+    for p in range(P):  # every model placed on one or two groups
+        for m in range(hm.shape[1]):
+            bits = 1 << int(rng.integers(0, 4))
+            if rng.random() < 0.5:
+                bits |= 1 << int(rng.integers(0, 4))
+            hm[p, m] = np.uint64(bits)
+    scales = [1.0, 2.0, 5.0, 10.0]
+    for B in (1, 2, 4, 8):
+        say("experiment workload B", B, len(pb.t))
+        served, digest, fin = _run(dev, pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat, gc, hm, scales,
+                                   B, 1.0, [3, 17])
+        _check(oracle.lib(), pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat, gc, hm, scales, B, 1.0,
+               served, digest, fin, [3, 17])
+
+
+def test_batching_empty_and_overflow(dev):
+    import torch
+    from paper_2302_11665_amd import sim
+    rng = np.random.default_rng(11)
+    t, model, d, cs, L, gc, hm = _case(rng, 2, 1, 3, 400)
+    served, digest, _ = _run(dev, t[:0], model[:0], d, cs, L, gc, hm, [2.0], 4, 1.0, [])
+    assert served.tolist() == [0] * gc.shape[0]
+    # a burst on one single-server group with an unlimited SLO: 300 requests
+    # queue at once, more than a 64-entry queue holds
+    tb = np.zeros(300)
+    mb = np.zeros(300, np.int32)
+    with pytest.raises(sim.SimError) as ei:
+        _run(dev, tb, mb, np.ones(1), np.array([1], np.int32), np.ones((1, 1, 1)), np.zeros((1, 1), np.int32),
+             np.ones((1, 1), np.uint64), [INF], 4, 1.0, [], qcap=64)
+    assert ei.value.code == sim.AS_E_LIMITS
+    served, digest, fin = _run(dev, tb, mb, np.ones(1), np.array([1], np.int32), np.ones((1, 1, 1)),
+                               np.zeros((1, 1), np.int32), np.ones((1, 1), np.uint64), [INF], 4, 1.0, [0], qcap=512)
+    s, dg, ofin, _ = oracle.lib().simulate_job_batched(tb, mb, np.ones(1), np.array([1], np.int32), np.ones((1, 1, 1)),
+                                                       np.zeros(1, np.int32), np.ones(1, np.uint64), INF, 4, 1.0)
+    assert int(served[0]) == s == 300 and fin[0].tobytes() == ofin.tobytes()
