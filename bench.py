@@ -19,9 +19,12 @@ point with its own 10-minute trace (4096 segments, about 4.4e8 requests) --
 timed the same way, with its HBM roofline (each segment is read once).
 
 And, as "search": wall time and simulated events of two placement searches
-(reduced and full Alg. 2) on the 32-model / 64-device workload.
+(reduced and full Alg. 2) on the 32-model / 64-device workload; as
+"batching": the dynamic-batching simulator on the batching experiment's shape
+for maximum batch sizes 1-8.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep] [--no-search]
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep]
+                    [--no-search] [--no-batching]
 """
 import argparse
 import json
@@ -213,6 +216,63 @@ def bench_search(args, np, torch, sim, problems):
     return out
 
 
+def bench_batching(args, np, torch, sim, problems):
+    """The dynamic-batching simulator (Sec. 6.5) on the batching experiment's
+    shape: 32 models of 151 ms, Gamma 4 req/s per model CV 4 for 10 minutes,
+    256 placements on 16 groups of 4 devices (S=4) x 8 SLO scales, for maximum
+    batch sizes 1, 2, 4 and 8 at latency slope 1; each call timed with HIP
+    events, plus the oracle's rate on a sample of jobs with sampled parity."""
+    import oracle
+    pb = problems.batching()
+    N, J = len(pb.t), pb.n_jobs
+    d = sim.to_device
+    t, m, ds, L, gc, hm, sc = (d(pb.t), d(pb.model), d(pb.d_single), d(pb.stage_lat), d(pb.group_cfg),
+                               d(pb.host_mask), d(pb.slo_scale))
+    served = torch.empty(J, dtype=torch.int64, device="cuda")
+    digest = torch.empty((J, 2), dtype=torch.int64, device="cuda")
+    K = len(pb.slo_scale)
+    out = {"workload": "batching experiment shape: 32 models x 151 ms, Gamma 4 req/s/model CV 4, 600 s; "
+                       "256 placements of 16 groups (S=4) x 8 SLO scales 1..20; latency slope 1",
+           "requests": N, "jobs": J, "events_per_call": N * J, "by_max_batch": {}}
+    lib = oracle.lib() if not args.no_cpu else None
+    sample = list(range(0, J, max(1, J // 8)))[:8]
+    for B in (1, 2, 4, 8):
+        call = lambda: sim.as_simulate_batched(t, m, ds, pb.cfg_stages, L, gc, hm, sc, B, 1.0, served, digest,
+                                               queue_cap=128)
+        try:
+            call()
+        except sim.SimError as e:
+            out["by_max_batch"][str(B)] = {"error": str(e)}
+            log(f"batching B={B}: {e}")
+            continue
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        for k in range(3):
+            call()
+            ev[k + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.mean([ev[k].elapsed_time(ev[k + 1]) for k in range(3)]))
+        s_np, dg = served.cpu().numpy(), sim.u64(digest)
+        res = {"ms_per_call": round(ms, 3), "events_per_s": round(N * J / (ms / 1000.0), 1),
+               "attainment_mean": round(float(s_np.sum()) / (N * J), 5)}
+        if lib is not None:
+            t0 = time.perf_counter()
+            mism = 0
+            for j in sample:
+                p, k = divmod(j, K)
+                so, dgo, _, _ = lib.simulate_job_batched(pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat,
+                                                         pb.group_cfg[p], pb.host_mask[p], pb.slo_scale[k], B, 1.0)
+                mism += int(so != int(s_np[j]) or dgo != tuple(int(x) for x in dg[j]))
+            cpu_s = time.perf_counter() - t0
+            res["cpu_oracle_events_per_s"] = round(len(sample) * N / cpu_s, 1)
+            res["parity_sampled"] = {"jobs": len(sample), "mismatches": mism}
+        log(f"batching B={B}: {ms:.2f} ms/call, mean attainment {res['attainment_mean']}")
+        out["by_max_batch"][str(B)] = res
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -224,6 +284,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true", help="skip the SLO-curve sweep workload")
     ap.add_argument("--no-search", action="store_true", help="skip the placement-search timings")
+    ap.add_argument("--no-batching", action="store_true", help="skip the dynamic-batching timings")
     ap.add_argument("--sweep-only", action="store_true",
                     help="time only the SLO-curve sweep (prints its object alone)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
@@ -342,6 +403,8 @@ def main():
         out["sweep"] = bench_sweep(args, np, torch, api, problems)
     if not args.no_search:
         out["search"] = bench_search(args, np, torch, sim, problems)
+    if not args.no_batching:
+        out["batching"] = bench_batching(args, np, torch, sim, problems)
     print(json.dumps(out), flush=True)
 
 

@@ -60,22 +60,30 @@ __device__ __forceinline__ double rl_f64(double v, int lane) {
   return __hiloint2double(hi, lo);
 }
 
-// LDS of one job: queue entries [M][qcap], heads and tails [M], SLOs [M],
-// stage-latency table [M][Cp][SMAX].
+constexpr int kBatchChunk = 512;  // trace requests staged per LDS refill
+
+// LDS of one job: queue entries (trace index and deadline) [M][qcap], heads
+// and tails [M], SLOs [M], stage-latency table [M][Cp][SMAX], trace chunk.
 __host__ __device__ constexpr size_t batch_lds_bytes(int M, int Cp, int SMAX, int qcap) {
-  return (size_t)M * qcap * 4 + (size_t)M * 8 + (size_t)M * 8 + (size_t)M * Cp * SMAX * 8;
+  return (size_t)M * qcap * 12 + (size_t)M * 8 + (size_t)M * 8 + (size_t)M * Cp * SMAX * 8 +
+         (size_t)kBatchChunk * 12;
 }
 
-template <int SMAX>
+// W: lanes reduced per job, the group count rounded up to a power of two (at
+// least 16, so the reductions inside a 16-lane row are DPP only).
+template <int W, int SMAX>
 __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   int cp = 1;
   while (cp < a.C) cp <<= 1;
-  double* sL = reinterpret_cast<double*>(smem);               // [M][cp][SMAX]
-  double* sSlo = sL + (size_t)a.M * cp * SMAX;                  // [M]
-  uint32_t* sHead = reinterpret_cast<uint32_t*>(sSlo + a.M);    // [M]
-  uint32_t* sTail = sHead + a.M;                                // [M]
-  uint32_t* sQ = sTail + a.M;                                   // [M][qcap]
+  double* sL = reinterpret_cast<double*>(smem);                   // [M][cp][SMAX]
+  double* sSlo = sL + (size_t)a.M * cp * SMAX;                    // [M]
+  double* sQd = sSlo + a.M;                                       // [M][qcap] deadlines
+  double* sT = sQd + (size_t)a.M * a.qcap;                        // chunk times
+  uint32_t* sHead = reinterpret_cast<uint32_t*>(sT + kBatchChunk);  // [M]
+  uint32_t* sTail = sHead + a.M;                                  // [M]
+  uint32_t* sQi = sTail + a.M;                                    // [M][qcap] trace indices
+  int32_t* sM = reinterpret_cast<int32_t*>(sQi + (size_t)a.M * a.qcap);  // chunk models
   const int lane = threadIdx.x;
   const int64_t job = blockIdx.x;
   const int p = (int)(job / a.K);
@@ -130,115 +138,152 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
     }
     return f;
   };
+  // smallest key over the job's lanes (lane 0's segment), wave-uniform
+  auto wave_min = [&](double key) {
+    const double v = seg_min<W>(key);
+    return rl_f64(v, 0);
+  };
 
-  for (int64_t i = 0; i <= a.n; ++i) {
-    const bool last = i == a.n;
-    const double horizon = last ? 0.0 : a.t[i];
-    // idle events up to the arrival (all remaining ones after the last)
-    for (;;) {
-      const bool work = cfg >= 0 && (hostbits & nonempty) != 0;
-      const double key = work ? F[0] : kInf;
-      const double mn = seg_min<64>(key);
-      const uint64_t wm = __builtin_amdgcn_ballot_w64(work && key == mn);
-      if (wm == 0) break;
-      if (!last && !(mn <= horizon)) break;
-      const int g = __builtin_ctzll(wm);
-      const uint64_t ghost = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(hostbits >> 32), g) << 32) |
-                             (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)hostbits, g);
-      for (;;) {
-        uint64_t cand = ghost & nonempty;
-        if (cand == 0) break;  // nothing left for this group: it stays idle
-        int mc = -1;
-        uint32_t hidx = 0;
-        while (cand) {
-          const int m = __builtin_ctzll(cand);
-          cand &= cand - 1;
-          const uint32_t r = sQ[(size_t)m * a.qcap + (sHead[m] & qmask)];
-          if (mc < 0 || r < hidx) {
-            mc = m;
-            hidx = r;
-          }
-        }
-        const double dl = a.t[hidx] + sSlo[mc];
-        const uint32_t avail = sTail[mc] - sHead[mc];
-        const int bmax = (int)(avail < (uint32_t)a.max_batch ? avail : (uint32_t)a.max_batch);
-        int b = 0;
-        double fin = 0.0;
-        double fs[SMAX];
-        for (int bb = 1; bb <= bmax; ++bb) {
-          double fsb[SMAX];
-          const double fl = rl_f64(chain(mc, bb, mn, fsb), g);
-          if (fl > dl) break;
-          b = bb;
-          fin = fl;
-#pragma unroll
-          for (int s = 0; s < SMAX; ++s) fs[s] = fsb[s];
-        }
-        if (b == 0) {
-          // the head cannot meet its deadline: dropped (its output stays -1)
-          __syncthreads();
-          if (lane == 0) sHead[mc] += 1;
-          __syncthreads();
-          if (sHead[mc] == sTail[mc]) nonempty &= ~(1ull << mc);
-          continue;
-        }
-        if (lane == g) {
-#pragma unroll
-          for (int s = 0; s < SMAX; ++s) F[s] = fs[s];
-        }
-        const uint32_t h0 = sHead[mc];
-        for (int k = 0; k < b; ++k) {
-          const uint32_t r = sQ[(size_t)mc * a.qcap + ((h0 + k) & qmask)];
-          h += mix64(r);
-          fin_sum += (uint64_t)__double_as_longlong(fin);
-          if (frowp && lane == 0) frowp[r] = fin;
-        }
-        served += b;
-        __syncthreads();
-        if (lane == 0) sHead[mc] = h0 + b;
-        __syncthreads();
-        if (h0 + b == sTail[mc]) nonempty &= ~(1ull << mc);
-        break;
-      }
+  for (int64_t base = 0; base <= a.n; base += kBatchChunk) {
+    const int cnt = (int)((a.n - base) < kBatchChunk ? (a.n - base) : kBatchChunk);
+    __syncthreads();
+    for (int e = lane; e < cnt; e += 64) {
+      sT[e] = a.t[base + e];
+      sM[e] = a.model[base + e];
     }
-    if (last) break;
-    // the arrival
-    const double ti = horizon;
-    const int m0 = a.model[i];
-    const bool mok = (unsigned)m0 < (unsigned)a.M;
-    const int m = mok ? m0 : 0;
-    const bool hosted = mok && cfg >= 0 && ((hostbits >> m) & 1u);
-    if (__builtin_amdgcn_ballot_w64(hosted) == 0) continue;  // no group hosts it: a miss
-    const bool avail = hosted && F[0] <= ti;
-    const double key = avail ? F[0] : kInf;
-    const double mn = seg_min<64>(key);
-    const uint64_t am = __builtin_amdgcn_ballot_w64(avail && key == mn);
-    if (am != 0) {
-      const int ga = __builtin_ctzll(am);
-      double fs[SMAX];
-      const double fl = rl_f64(chain(m, 1, ti, fs), ga);
-      if (!(fl > ti + sSlo[m])) {
-        if (lane == ga) {
+    __syncthreads();
+    // cnt requests of this chunk, then (after the last one) the final drain
+    const int steps = base + kBatchChunk > a.n ? cnt + 1 : cnt;
+    for (int e = 0; e < steps; ++e) {
+      const bool last = e == cnt;
+      const int64_t i = base + e;
+      const double horizon = last ? 0.0 : sT[e];
+      // idle events up to the arrival (all remaining ones after the last)
+      for (;;) {
+        const bool work = cfg >= 0 && (hostbits & nonempty) != 0;
+        const double key = work ? F[0] : kInf;
+        const double mn = wave_min(key);
+        const uint64_t wm = __builtin_amdgcn_ballot_w64(work && key == mn);
+        if (wm == 0) break;
+        if (!last && !(mn <= horizon)) break;
+        const int g = __builtin_ctzll(wm);
+        const uint64_t ghost = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(hostbits >> 32), g) << 32) |
+                               (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)hostbits, g);
+        for (;;) {
+          uint64_t cand = ghost & nonempty;
+          if (cand == 0) break;  // nothing left for this group: it stays idle
+          int mc = -1;
+          uint32_t hidx = 0;
+          while (cand) {
+            const int m = __builtin_ctzll(cand);
+            cand &= cand - 1;
+            const uint32_t r = sQi[(size_t)m * a.qcap + (sHead[m] & qmask)];
+            if (mc < 0 || r < hidx) {
+              mc = m;
+              hidx = r;
+            }
+          }
+          const uint32_t h0 = sHead[mc];
+          const double dl = sQd[(size_t)mc * a.qcap + (h0 & qmask)];
+          const uint32_t avail = sTail[mc] - h0;
+          const int bmax = (int)(avail < (uint32_t)a.max_batch ? avail : (uint32_t)a.max_batch);
+          int b = 0;
+          double fin = 0.0;
+          double fs[SMAX];
+          for (int bb = 1; bb <= bmax; ++bb) {
+            double fsb[SMAX];
+            const double fl = rl_f64(chain(mc, bb, mn, fsb), g);
+            if (fl > dl) break;
+            b = bb;
+            fin = fl;
 #pragma unroll
-          for (int s = 0; s < SMAX; ++s) F[s] = fs[s];
+            for (int s = 0; s < SMAX; ++s) fs[s] = fsb[s];
+          }
+          if (b == 0) {
+            // the head cannot meet its deadline: dropped (its output stays -1)
+            __syncthreads();
+            if (lane == 0) sHead[mc] = h0 + 1;
+            __syncthreads();
+            if (h0 + 1 == sTail[mc]) nonempty &= ~(1ull << mc);
+            continue;
+          }
+          if (lane == g) {
+#pragma unroll
+            for (int s = 0; s < SMAX; ++s) F[s] = fs[s];
+          }
+          for (int k = 0; k < b; ++k) {
+            const uint32_t r = sQi[(size_t)mc * a.qcap + ((h0 + k) & qmask)];
+            h += mix64(r);
+            fin_sum += (uint64_t)__double_as_longlong(fin);
+            if (frowp && lane == 0) frowp[r] = fin;
+          }
+          served += b;
+          __syncthreads();
+          if (lane == 0) sHead[mc] = h0 + b;
+          __syncthreads();
+          if (h0 + b == sTail[mc]) nonempty &= ~(1ull << mc);
+          break;
         }
-        served += 1;
-        h += mix64((uint64_t)i);
-        fin_sum += (uint64_t)__double_as_longlong(fl);
-        if (frowp && lane == 0) frowp[i] = fl;
       }
-    } else {
-      const uint32_t tl = sTail[m];
-      if (tl - sHead[m] == (uint32_t)a.qcap) {
-        if (lane == 0) atomicOr(a.overflow, 1u);  // queue full: the request is lost
-      } else {
-        __syncthreads();
-        if (lane == 0) {
-          sQ[(size_t)m * a.qcap + (tl & qmask)] = (uint32_t)i;
-          sTail[m] = tl + 1;
+      if (last) break;
+      // the arrival
+      const double ti = horizon;
+      const int m0 = sM[e];
+      const bool mok = (unsigned)m0 < (unsigned)a.M;
+      const int m = mok ? m0 : 0;
+      const bool hosted = mok && cfg >= 0 && ((hostbits >> m) & 1u);
+      if (__builtin_amdgcn_ballot_w64(hosted) == 0) continue;  // no group hosts it: a miss
+      const bool avail = hosted && F[0] <= ti;
+      const uint64_t av = __builtin_amdgcn_ballot_w64(avail);
+      if (av != 0) {
+        const double key = avail ? F[0] : kInf;
+        const double mn = wave_min(key);
+        const int ga = __builtin_ctzll(__builtin_amdgcn_ballot_w64(avail && key == mn));
+        double fs[SMAX];
+        const double fl = rl_f64(chain(m, 1, ti, fs), ga);
+        if (!(fl > ti + sSlo[m])) {
+          if (lane == ga) {
+#pragma unroll
+            for (int s = 0; s < SMAX; ++s) F[s] = fs[s];
+          }
+          served += 1;
+          h += mix64((uint64_t)i);
+          fin_sum += (uint64_t)__double_as_longlong(fl);
+          if (frowp && lane == 0) frowp[i] = fl;
         }
-        __syncthreads();
-        nonempty |= 1ull << m;
+      } else {
+        // Queue heads of model m that can no longer be served are dropped
+        // now rather than when a group reaches them: any batch that could
+        // still serve a queued request starts at or after ti, so it finishes
+        // no earlier than the chain from ti through a hosting group's stages
+        // with single-request latencies, free times ignored (fp64 rounding
+        // is monotone); a head whose deadline lies before the smallest such
+        // bound is dropped by the definition too, and dropping it earlier
+        // changes no other decision.  This keeps each queue to the requests
+        // that are still servable.
+        double lbv = ti;
+        {
+          const double* L = lbase + (size_t)m * cp * SMAX;
+#pragma unroll
+          for (int s = 0; s < SMAX; ++s) lbv = lbv + L[s];
+        }
+        const double lb = wave_min(hosted ? lbv : kInf);
+        uint32_t hd = sHead[m];
+        const uint32_t tl = sTail[m];
+        while (hd != tl && sQd[(size_t)m * a.qcap + (hd & qmask)] < lb) ++hd;
+        if (tl - hd == (uint32_t)a.qcap) {
+          if (lane == 0) atomicOr(a.overflow, 1u);  // queue full: the request is lost
+        } else {
+          __syncthreads();
+          if (lane == 0) {
+            sHead[m] = hd;
+            sQi[(size_t)m * a.qcap + (tl & qmask)] = (uint32_t)i;
+            sQd[(size_t)m * a.qcap + (tl & qmask)] = ti + sSlo[m];
+            sTail[m] = tl + 1;
+          }
+          __syncthreads();
+          nonempty |= 1ull << m;
+        }
       }
     }
   }
@@ -350,12 +395,23 @@ extern "C" int as_simulate_batched(const as_trace_t* trace, const as_models_t* m
     e = hipGetLastError();
   }
   if (e == hipSuccess) {
-    switch (smax) {
-      case 1: hipLaunchKernelGGL(as_dev::batch_kernel<1>, dim3((unsigned)J), dim3(64), lds, s, a); break;
-      case 2: hipLaunchKernelGGL(as_dev::batch_kernel<2>, dim3((unsigned)J), dim3(64), lds, s, a); break;
-      case 4: hipLaunchKernelGGL(as_dev::batch_kernel<4>, dim3((unsigned)J), dim3(64), lds, s, a); break;
-      default: hipLaunchKernelGGL(as_dev::batch_kernel<8>, dim3((unsigned)J), dim3(64), lds, s, a); break;
+    const int W = std::max(16, pow2ceil(a.G));
+    const dim3 grid((unsigned)J), block(64);
+#define AS_BATCH_LAUNCH(WW)                                                                         \
+  switch (smax) {                                                                                   \
+    case 1: hipLaunchKernelGGL((as_dev::batch_kernel<WW, 1>), grid, block, lds, s, a); break;       \
+    case 2: hipLaunchKernelGGL((as_dev::batch_kernel<WW, 2>), grid, block, lds, s, a); break;       \
+    case 4: hipLaunchKernelGGL((as_dev::batch_kernel<WW, 4>), grid, block, lds, s, a); break;       \
+    default: hipLaunchKernelGGL((as_dev::batch_kernel<WW, 8>), grid, block, lds, s, a); break;      \
+  }
+    if (W == 16) {
+      AS_BATCH_LAUNCH(16)
+    } else if (W == 32) {
+      AS_BATCH_LAUNCH(32)
+    } else {
+      AS_BATCH_LAUNCH(64)
     }
+#undef AS_BATCH_LAUNCH
     e = hipGetLastError();
   }
   uint32_t flag = 0;

@@ -338,3 +338,29 @@ def robustness(seed: int = 6, n_models: int = 16, n_devices: int = 16, device_me
                        np.array([k for _, k in cfgs], np.int32), L, parts, slo_scale,
                        {"devices": n_devices, "device_mem_mib": device_mem_gb * GIB_MIB})
     return RobustnessProblem(gp, tb, mb, {"a": (ra, ca), "b": (rb, cb), "window": window})
+
+
+def batching(seed: int = 7, n_models: int = 32, n_groups: int = 16, group_size: int = 4,
+             replicas: int = 4, n_placements: int = 256, duration: float = 600.0, rate: float = 4.0,
+             cv: float = 4.0, scales=(1.0, 1.5, 2.0, 3.0, 5.0, 7.5, 10.0, 20.0)) -> Problem:
+    """The shape of the batching experiment (Sec. 6.5): 32 instances of one
+    model (151 ms single-device latency, 2.4 GB, like Table 1's BERT-1.3B),
+    Gamma arrivals at 4 req/s per model with CV 4, ten minutes; 64 devices in
+    16 groups of 4 at (S=4, k=1); each placement puts every model on
+    `replicas` groups, the first of a seeded permutation of the groups (stream
+    (seed, permute, p*M + m)); 8 SLO scales from 1 to 20."""
+    M = n_models
+    d = np.full(M, 0.151)
+    w = np.full(M, int(2.4 * GIB_MIB), np.int64)
+    cfgs = [(group_size, 1)]
+    L = stage_table(d, cfgs)
+    t, m = gen.trace(seed, [rate] * M, cv, duration)
+    perms = gen.permutations(seed, gen.PURPOSE_PERMUTE, 0, n_placements * M, n_groups).reshape(
+        n_placements, M, n_groups)
+    hm = np.zeros((n_placements, M), np.uint64)
+    for r in range(replicas):
+        hm |= np.left_shift(np.uint64(1), perms[:, :, r].astype(np.uint64))
+    return Problem("batching", t, m, d, w, np.array([group_size], np.int32), np.array([1], np.int32), L,
+                   np.zeros((n_placements, n_groups), np.int32), hm, np.array(scales, np.float64),
+                   np.array([0, 8 * 100 + 4], np.int32),
+                   {"devices": n_groups * group_size})

@@ -114,7 +114,7 @@ def test_batching_experiment_workload(dev):
     for B in (1, 2, 4, 8):
         say("experiment workload B", B, len(pb.t))
         served, digest, fin = _run(dev, pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat, gc, hm, scales,
-                                   B, 1.0, [3, 17])
+                                   B, 1.0, [3, 17], qcap=256)
         _check(oracle.lib(), pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat, gc, hm, scales, B, 1.0,
                served, digest, fin, [3, 17])
 
