@@ -248,7 +248,8 @@ int as_partition_search(const as_trace_t* trace, const as_models_t* models,
  *                             configuration (the stage that bounds the
  *                             group's throughput, Sec. 3.4) is added to an
  *                             fp64 sum starting at 0
- * One job per wavefront (lane = group); meant for few jobs per call.  The
+ * With one scale the jobs run on the shared-trace kernel (lanes = groups,
+ * several jobs per wavefront); with several, one job per wavefront.  The
  * stage-latency table must fit in the LDS of a workgroup (AS_E_LIMITS
  * otherwise).
  */

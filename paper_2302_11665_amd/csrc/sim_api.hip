@@ -87,15 +87,16 @@ hipError_t launch_lds_any(int W, int gpl, int smax, bool seg, const KArgs& a, si
   }
 }
 
-hipError_t launch_shared_any(int W, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+hipError_t launch_shared_any(int W, int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s,
+                             bool stats) {
   switch (W) {
-    case 1: return as_host::launch_shared<1>(smax, usig, a, lds, s);
-    case 2: return as_host::launch_shared<2>(smax, usig, a, lds, s);
-    case 4: return as_host::launch_shared<4>(smax, usig, a, lds, s);
-    case 8: return as_host::launch_shared<8>(smax, usig, a, lds, s);
-    case 16: return as_host::launch_shared<16>(smax, usig, a, lds, s);
-    case 32: return as_host::launch_shared<32>(smax, usig, a, lds, s);
-    default: return as_host::launch_shared<64>(smax, usig, a, lds, s);
+    case 1: return as_host::launch_shared<1>(smax, usig, stats, a, lds, s);
+    case 2: return as_host::launch_shared<2>(smax, usig, stats, a, lds, s);
+    case 4: return as_host::launch_shared<4>(smax, usig, stats, a, lds, s);
+    case 8: return as_host::launch_shared<8>(smax, usig, stats, a, lds, s);
+    case 16: return as_host::launch_shared<16>(smax, usig, stats, a, lds, s);
+    case 32: return as_host::launch_shared<32>(smax, usig, stats, a, lds, s);
+    default: return as_host::launch_shared<64>(smax, usig, stats, a, lds, s);
   }
 }
 
@@ -308,6 +309,18 @@ __global__ void fill_seg_rows(const KArgs a) {
   }
 }
 
+// Statistics launch of the shared-trace kernel (one SLO scale, no per-request
+// rows): AS_E_LIMITS when its tables do not fit in a workgroup's LDS.
+int run_shared_stats(KArgs& a, int smax, hipStream_t stream) {
+  const int Ws = pow2ceil(a.G);
+  const size_t lds = as_dev::shared_lds_bytes(a.M, pow2ceil(a.C), smax) + as_dev::shared_stats_lds_bytes(Ws, a.M);
+  if (!use_shared_path() || a.K != 1 || a.n_finish != 0 || lds > shared_lds_limit())
+    return AS_E_LIMITS;
+  const hipError_t e = launch_shared_any(Ws, smax, true, a, lds, stream, true);
+  if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 // Launch the batched simulation of a shared trace (a fully filled except the
 // kernel shape).  W is the group count on entry.
 int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
@@ -328,7 +341,7 @@ int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
       if ((e = hipGetLastError()) != hipSuccess)
         return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     }
-    e = launch_shared_any(Ws, smax, a.K == 1, a, lds_shared, stream);
+    e = launch_shared_any(Ws, smax, a.K == 1, a, lds_shared, stream, false);
     if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     return ok();
   }

@@ -26,5 +26,9 @@ int check_common(const as_models_t* models, const as_placements_t* plc, KArgs& a
 // Launch the batched simulation of a shared trace; a is complete except for
 // the kernel shape, W is the group count on entry.
 int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream);
+// Statistics launch of the shared-trace kernel (one SLO scale, no per-request
+// output rows); returns AS_E_LIMITS without launching when that kernel cannot
+// take the call (several scales, output rows, tables beyond the LDS).
+int run_shared_stats(KArgs& a, int smax, hipStream_t stream);
 
 }  // namespace as_host

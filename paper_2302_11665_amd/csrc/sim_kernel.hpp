@@ -70,6 +70,8 @@ struct KArgs {
   uint64_t* out_digest;
   double* out_finish;
   int64_t finish_stride;
+  int64_t* out_model_served;  // statistics launches: [J][M]
+  double* out_group_busy;     // statistics launches: [J][G]
   int32_t M, C, smax_in, G, K, J, n_finish;
   int32_t P, n_segments;
   int32_t cfg_stages[AS_MAX_CONFIGS];

@@ -36,10 +36,13 @@ hipError_t lds_s(int smax, const KArgs& a, size_t lds, hipStream_t s) {
 }
 
 template <int W, int SMAX>
-hipError_t shared_t(bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+hipError_t shared_t(bool usig, bool stats, const KArgs& a, size_t lds, hipStream_t s) {
   constexpr int slots = (64 / W) * as_dev::kWaves;
   const int grid = (a.J + slots - 1) / slots;
-  if (usig)
+  if (stats)
+    hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, true, true>), dim3(grid), dim3(as_dev::kThreads),
+                       lds, s, a);
+  else if (usig)
     hipLaunchKernelGGL((as_dev::shared_kernel<W, SMAX, true>), dim3(grid), dim3(as_dev::kThreads),
                        lds, s, a);
   else
@@ -60,12 +63,12 @@ hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, h
 }
 
 template <int W>
-hipError_t launch_shared(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s) {
+hipError_t launch_shared(int smax, bool usig, bool stats, const KArgs& a, size_t lds, hipStream_t s) {
   switch (smax) {
-    case 1: return shared_t<W, 1>(usig, a, lds, s);
-    case 2: return shared_t<W, 2>(usig, a, lds, s);
-    case 4: return shared_t<W, 4>(usig, a, lds, s);
-    default: return shared_t<W, 8>(usig, a, lds, s);
+    case 1: return shared_t<W, 1>(usig, stats, a, lds, s);
+    case 2: return shared_t<W, 2>(usig, stats, a, lds, s);
+    case 4: return shared_t<W, 4>(usig, stats, a, lds, s);
+    default: return shared_t<W, 8>(usig, stats, a, lds, s);
   }
 }
 
@@ -91,6 +94,6 @@ hipError_t launch_seg64(int smax, const KArgs& a, size_t lds, hipStream_t s) {
 #endif
 
 template hipError_t launch_lds<AS_W>(int, int, bool, const KArgs&, size_t, hipStream_t);
-template hipError_t launch_shared<AS_W>(int, bool, const KArgs&, size_t, hipStream_t);
+template hipError_t launch_shared<AS_W>(int, bool, bool, const KArgs&, size_t, hipStream_t);
 
 }  // namespace as_host

@@ -14,9 +14,10 @@ using as_dev::KArgs;
 template <int W>
 hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, hipStream_t s);
 
-// Shared-trace kernel: one group per lane, USIG = one SLO scale for all jobs.
+// Shared-trace kernel: one group per lane, USIG = one SLO scale for all jobs;
+// stats (one scale only): per-model served counts and per-group busy time.
 template <int W>
-hipError_t launch_shared(int smax, bool usig, const KArgs& a, size_t lds, hipStream_t s);
+hipError_t launch_shared(int smax, bool usig, bool stats, const KArgs& a, size_t lds, hipStream_t s);
 
 // Segmented jobs with up to 64 groups, one job per wavefront (built in the
 // 64-lane unit).
@@ -24,7 +25,7 @@ hipError_t launch_seg64(int smax, const KArgs& a, size_t lds, hipStream_t s);
 
 #define AS_DECLARE_W(W)                                                                       \
   extern template hipError_t launch_lds<W>(int, int, bool, const KArgs&, size_t, hipStream_t); \
-  extern template hipError_t launch_shared<W>(int, bool, const KArgs&, size_t, hipStream_t);
+  extern template hipError_t launch_shared<W>(int, bool, bool, const KArgs&, size_t, hipStream_t);
 AS_DECLARE_W(1)
 AS_DECLARE_W(2)
 AS_DECLARE_W(4)

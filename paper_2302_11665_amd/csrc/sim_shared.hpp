@@ -108,6 +108,7 @@ struct SharedLane {
   double F[SMAX];
   uint64_t fin_sum, hash, served;
   uint32_t wlo;
+  double busy;  // statistics launches: this lane's group's busy time
 };
 
 struct SharedConst {
@@ -121,6 +122,7 @@ struct SharedConst {
                              // the element of the chunk's first request
   int64_t flimit;            // requests i < flimit have an output element
   int fcnt;                  // within a chunk: its first fcnt requests have one
+  uint32_t* cnt;             // statistics launches: this job's per-model served counters (LDS)
 };
 
 // Projection through this lane's stage chain (Sec. 3.4): fs[s] is the
@@ -140,10 +142,10 @@ __device__ __forceinline__ double chain(const SharedLane<SMAX>& st, double ti,
 // One request, number ik of its chunk.  hm: the wavefront's hosting lanes; cnt:
 // the record's count; L: this lane's stage latencies of the model; dv: the
 // deadline t + SLO (USIG, staged with the trace) or d_single of the model.
-template <int W, int SMAX, bool USIG, bool FINISH, bool FLIM>
+template <int W, int SMAX, bool USIG, bool FINISH, bool FLIM, bool STATS = false>
 __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedConst& c, double ti,
                                           uint64_t hm, uint32_t cnt, const double (&L)[SMAX],
-                                          double dv, int ik, uint32_t& sr) {
+                                          double dv, int ik, uint32_t& sr, int mi = 0) {
   uint64_t cm = hm;  // the dispatch target of every job: one lane per job or none
   if (cnt != 0) {
     const bool hosted = __builtin_amdgcn_inverse_ballot_w64(hm);
@@ -171,6 +173,17 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
   for (int s = 0; s < SMAX; ++s) st.F[s] = acc ? fs[s] : st.F[s];
   st.fin_sum += acc ? (uint64_t)__double_as_longlong(f) : 0ull;
   sr = (sr << 1) | (acc ? 1u : 0u);
+  if constexpr (STATS) {
+    // the accepting lane's group was busy for the model's slowest stage
+    // (fp64 sum in trace order) and served one more request of it
+    double slowest = 0.0;
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) slowest = vmax(slowest, L[s]);
+    if (acc) {
+      st.busy += slowest;
+      atomicAdd(c.cnt + mi, 1u);
+    }
+  }
   if constexpr (FINISH) {
     // per-request output: the job's target lane writes the finish time, or
     // -1 if rejected; rows start filled with -2 (a request no group hosts)
@@ -184,7 +197,7 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
 // together), then run them in order.  UNI: every group of the wavefront has
 // the same configuration, whose stage latencies the model records hold;
 // otherwise each lane reads its configuration's row.
-template <int W, int SMAX, int B, bool USIG, bool FINISH, bool FLIM, bool UNI>
+template <int W, int SMAX, int B, bool USIG, bool FINISH, bool FLIM, bool UNI, bool STATS = false>
 __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedConst& c,
                                            const double* __restrict__ cTD,
                                            const uint32_t* __restrict__ cO, int i0, uint32_t& sr) {
@@ -226,13 +239,14 @@ __device__ __forceinline__ void fast_batch(SharedLane<SMAX>& st, const SharedCon
     const uint64_t hm = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(hmv[k] >> 32)) << 32) |
                         (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)hmv[k]);
     const uint32_t cnt = (uint32_t)__builtin_amdgcn_readfirstlane((int)cnv[k]);
-    fast_step<W, SMAX, USIG, FINISH, FLIM>(st, c, t[k], hm, cnt, L[k], dv[k], i0 + k, sr);
+    fast_step<W, SMAX, USIG, FINISH, FLIM, STATS>(st, c, t[k], hm, cnt, L[k], dv[k], i0 + k, sr,
+                                                  (int)(off[k] >> rec_shift(SMAX)));
   }
 }
 
 // All requests of one LDS chunk [base, base + cnt): 32-request halves of
 // 64-request accept words.
-template <int W, int SMAX, bool USIG, bool FINISH, bool FLIM, bool UNI>
+template <int W, int SMAX, bool USIG, bool FINISH, bool FLIM, bool UNI, bool STATS = false>
 __device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedConst& c0,
                                            const double* __restrict__ cTD,
                                            const uint32_t* __restrict__ cO, int cnt, int64_t base,
@@ -253,10 +267,10 @@ __device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedCon
     uint32_t sr = 0;
     if (hc == 32) {
       for (int e = 0; e < 32; e += B)
-        fast_batch<W, SMAX, B, USIG, FINISH, FLIM, UNI>(st, c, cTD + 2 * (h + e), cO + h + e, h + e, sr);
+        fast_batch<W, SMAX, B, USIG, FINISH, FLIM, UNI, STATS>(st, c, cTD + 2 * (h + e), cO + h + e, h + e, sr);
     } else {
       for (int e = 0; e < hc; ++e)
-        fast_batch<W, SMAX, 1, USIG, FINISH, FLIM, UNI>(st, c, cTD + 2 * (h + e), cO + h + e, h + e, sr);
+        fast_batch<W, SMAX, 1, USIG, FINISH, FLIM, UNI, STATS>(st, c, cTD + 2 * (h + e), cO + h + e, h + e, sr);
     }
     const int64_t pos = (base + h) & 63;  // 0 or 32
     const bool end = base + h + hc == n;
@@ -283,9 +297,16 @@ __host__ __device__ constexpr size_t shared_lds_bytes(int M, int Cp, int SMAX) {
          (size_t)kChunk * 20;
 }
 
+// Statistics launches (STATS, one SLO scale) also count each job's served
+// requests per model (LDS counters after the chunk) and sum each group's busy
+// time, for the fast placement heuristic.
+__host__ __device__ constexpr size_t shared_stats_lds_bytes(int W, int M) {
+  return (size_t)kWaves * (64 / W) * M * 4;
+}
+
 // Jobs of workgroup b: wavefront v holds jobs b*kWaves*JW + v*JW + lane/W,
 // JW = 64/W.  Per-request output rows must hold -2 when the kernel starts.
-template <int W, int SMAX, bool USIG>
+template <int W, int SMAX, bool USIG, bool STATS = false>
 __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   constexpr int JW = 64 / W;
   constexpr int kSlots = JW * kWaves;
@@ -381,6 +402,12 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
   st.fin_sum = st.hash = st.served = 0;
   st.wlo = 0;
+  st.busy = 0.0;
+  uint32_t* sCnt = sO + kChunk;  // STATS: [kWaves * JW][M]
+  if constexpr (STATS) {
+    for (int idx = lane; idx < JW * a.M; idx += 64) sCnt[(size_t)wave * JW * a.M + idx] = 0;
+    c.cnt = sCnt + ((size_t)wave * JW + lane / W) * a.M;
+  }
 
   const int64_t n = a.n;
   for (int64_t base = 0; base < n; base += kChunk) {
@@ -396,7 +423,13 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
       sO[e] = off;
     }
     __syncthreads();
-    if (uni) {
+    if constexpr (STATS) {
+      // statistics launches carry no per-request output rows
+      if (uni)
+        fast_chunk<W, SMAX, USIG, false, false, true, true>(st, c, sTD, sO, cnt, base, n);
+      else
+        fast_chunk<W, SMAX, USIG, false, false, false, true>(st, c, sTD, sO, cnt, base, n);
+    } else if (uni) {
       if (wave_finish)
         fast_chunk<W, SMAX, USIG, true, false, true>(st, c, sTD, sO, cnt, base, n);
       else
@@ -417,6 +450,11 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
       a.out_digest[2 * job] = st.hash;
       a.out_digest[2 * job + 1] = fin_sum;
     }
+  }
+  if constexpr (STATS) {
+    if (job_ok && seg_lane < a.G && a.out_group_busy) a.out_group_busy[job * a.G + seg_lane] = st.busy;
+    if (job_ok && a.out_model_served)
+      for (int m = seg_lane; m < a.M; m += W) a.out_model_served[job * a.M + m] = (int64_t)c.cnt[m];
   }
 }
 

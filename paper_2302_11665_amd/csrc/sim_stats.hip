@@ -200,6 +200,24 @@ extern "C" int as_simulate_stats(const as_trace_t* trace, const as_models_t* mod
   if (J > 0 && (!slo_scale || !out_served))
     return fail(AS_E_INVALID_ARG, "slo_scale and out_served must not be NULL");
   if (J == 0) return ok();
+  hipStream_t s = (hipStream_t)stream;
+  if (n_scales == 1) {
+    // one scale: the tuned shared-trace kernel with its statistics outputs
+    ka.t = trace->t;
+    ka.model = trace->model;
+    ka.n = trace->n;
+    ka.slo_scale = slo_scale;
+    ka.K = 1;
+    ka.J = (int32_t)J;
+    ka.P = placements->n_placements;
+    ka.out_served = out_served;
+    ka.out_digest = out_digest;
+    ka.out_model_served = out_model_served;
+    ka.out_group_busy = out_group_busy;
+    ka.n_finish = 0;
+    const int r = run_shared_stats(ka, smax, s);
+    if (r != AS_E_LIMITS) return r;
+  }
   as_dev::StatsArgs a;
   std::memset(&a, 0, sizeof a);
   a.t = trace->t;
@@ -226,7 +244,6 @@ extern "C" int as_simulate_stats(const as_trace_t* trace, const as_models_t* mod
     return fail(AS_E_LIMITS, "stage-latency table (%d models x %d configs x %d stages) does not fit in LDS",
                 a.M, a.C, smax);
   const int grid = (int)((J + as_dev::kWaves - 1) / as_dev::kWaves);
-  hipStream_t s = (hipStream_t)stream;
   switch (smax) {
     case 1: hipLaunchKernelGGL(as_dev::stats_kernel<1>, dim3(grid), dim3(as_dev::kThreads), lds, s, a); break;
     case 2: hipLaunchKernelGGL(as_dev::stats_kernel<2>, dim3(grid), dim3(as_dev::kThreads), lds, s, a); break;

@@ -52,13 +52,18 @@ def _stats_case(rng, G, Smax, M, n):
     return t, model, d_single, cfg_stages, L, group_cfg, host_mask, scales
 
 
+# one scale runs the shared-trace kernel's statistics mode, several scales the
+# statistics kernel
+@pytest.mark.parametrize("one_scale", [True, False])
 @pytest.mark.parametrize("G,Smax", [(1, 1), (3, 2), (16, 4), (17, 3), (40, 8), (64, 1)])
-def test_stats_kernel_matches_oracle(dev, G, Smax):
+def test_stats_kernel_matches_oracle(dev, G, Smax, one_scale):
     import torch
     rng = np.random.default_rng(100 + G * 10 + Smax)
     M = 7
     n = 2500 + 7 * G
     t, model, d_single, cfg_stages, L, gcfg, hm, scales = _stats_case(rng, G, Smax, M, n)
+    if one_scale:
+        scales = scales[:1]
     say("stats", G, Smax, n)
     d = dev.to_device
     P, K = gcfg.shape[0], scales.shape[0]
