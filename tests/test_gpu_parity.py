@@ -233,3 +233,44 @@ def test_c4_full_size_sampled(gpu_api):
                                                                            int(pb.finish_jobs[-1])})
     fins = [int(pb.finish_jobs[0]), int(pb.finish_jobs[-1])]
     compare(res, oracle_problem(pb, jobs=jobs, finish_jobs=fins), len(pb.t), "c4 full sampled")
+
+
+def test_maximum_sizes(gpu):
+    """64 models, 64 groups, 8-stage pipelines, 8 configurations (the largest
+    stage-latency table every kernel shape holds), every job of several scales,
+    a ragged trace."""
+    rng = np.random.default_rng(64)
+    from paper_2302_11665_amd.workload.problems import Problem
+    M, G, S, C, n, P = 64, 64, 8, 8, 3001, 6
+    cfg_stages = rng.integers(1, S + 1, C).astype(np.int32)
+    cfg_stages[0] = S
+    L = rng.uniform(0.01, 0.4, (M, C, S))
+    gaps = rng.exponential(0.002, n)
+    gaps[rng.random(n) < 0.2] = 0.0
+    t = np.cumsum(gaps)
+    model = rng.integers(0, M, n).astype(np.int32)
+    gcfg = rng.integers(0, C, (P, G)).astype(np.int32)
+    masks = rng.integers(0, 1 << 62, (P, M)).astype(np.uint64) | rng.integers(0, 4, (P, M)).astype(np.uint64) << np.uint64(62)
+    d = L[:, 0, :].sum(axis=1) * rng.uniform(0.5, 1.5, M)
+    pb = Problem("maximum", t, model, d, np.zeros(M, np.int64), cfg_stages, np.ones(C, np.int32), L, gcfg, masks,
+                 np.array([0.0, 2.0, np.inf]), np.array([0, 7, 17], np.int32))
+    say("maximum sizes", M, G, S, C, n, P)
+    res = gpu.simulate_problem(pb)
+    compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), n, "maximum sizes")
+
+
+def test_table_beyond_lds_is_refused(gpu_api):
+    """64 models x 32 configurations x 8 stages do not fit in any kernel's LDS:
+    the call returns AS_E_LIMITS and launches nothing."""
+    import torch
+    from paper_2302_11665_amd import sim
+    M, C, S, G = 64, 32, 8, 4
+    d = sim.to_device
+    L = np.full((M, C, S), 0.1)
+    out = torch.zeros(1, dtype=torch.int64, device="cuda")
+    with pytest.raises(sim.SimError) as ei:
+        sim.as_simulate_placements(d(np.zeros(10)), d(np.zeros(10, np.int32)), d(np.ones(M)),
+                                   np.full(C, S, np.int32), d(L), d(np.zeros((1, G), np.int32)),
+                                   d(np.ones((1, M), np.uint64)), d(np.array([1.0])), out)
+    assert ei.value.code == sim.AS_E_LIMITS
+    assert int(out.cpu()[0]) == 0
