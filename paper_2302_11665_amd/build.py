@@ -25,6 +25,7 @@ SIM_SEARCH_SRC = os.path.join(CSRC, "sim_search.hip")
 SIM_STATS_SRC = os.path.join(CSRC, "sim_stats.hip")
 SIM_ALG2_SRC = os.path.join(CSRC, "sim_alg2.hip")
 SIM_BATCH_SRC = os.path.join(CSRC, "sim_batch.hip")
+SIM_SPEC_SRC = os.path.join(CSRC, "sim_spec.hip")
 LANE_WIDTHS = (1, 2, 4, 8, 16, 32, 64)  # one launcher translation unit per width
 SIM_LIB = os.path.join(BUILD, "libalpaserve_sim.so")
 
@@ -67,7 +68,8 @@ def build_sim(extra_flags=(), jobs=None) -> str:
              (SIM_SEARCH_SRC, os.path.join(obj_dir, "sim_search.o"), []),
              (SIM_STATS_SRC, os.path.join(obj_dir, "sim_stats.o"), []),
              (SIM_ALG2_SRC, os.path.join(obj_dir, "sim_alg2.o"), []),
-             (SIM_BATCH_SRC, os.path.join(obj_dir, "sim_batch.o"), [])]
+             (SIM_BATCH_SRC, os.path.join(obj_dir, "sim_batch.o"), []),
+             (SIM_SPEC_SRC, os.path.join(obj_dir, "sim_spec.o"), [])]
     for w in LANE_WIDTHS:
         units.append((SIM_LAUNCH_SRC, os.path.join(obj_dir, f"sim_launch_w{w}.o"), [f"-DAS_W={w}"]))
 

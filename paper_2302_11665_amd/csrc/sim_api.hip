@@ -153,10 +153,19 @@ bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, in
 }
 
 // Which kernel family runs a shared-trace call: the scalar path by default;
-// ALPASERVE_PATH=lds selects the LDS-staged kernel (used by tests to cover both).
+// ALPASERVE_PATH=lds selects the LDS-staged kernel, =spec the
+// segment-speculative one, =shared the shared-trace one (tests cover each).
 bool use_shared_path() {
   const char* e = getenv("ALPASERVE_PATH");
   return !(e && std::strcmp(e, "lds") == 0);
+}
+
+bool want_spec(const KArgs& a, int smax) {
+  (void)smax;
+  const char* e = getenv("ALPASERVE_PATH");
+  if (e && *e) return std::strcmp(e, "spec") == 0;
+  (void)a;
+  return false;
 }
 
 // Checks shared by both simulate entry points; fills the model/placement part
@@ -325,6 +334,10 @@ int run_shared_stats(KArgs& a, int smax, hipStream_t stream) {
 // kernel shape).  W is the group count on entry.
 int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
   const int64_t J = a.J;
+  if (want_spec(a, smax)) {
+    const int rc = run_spec(a, smax, stream);
+    if (rc != AS_E_LIMITS) return rc;
+  }
   // shared-trace kernel (one group per lane, W = G rounded up to a power of
   // two) unless its tables exceed the LDS of a workgroup; then the general
   // kernel, whose tables are smaller

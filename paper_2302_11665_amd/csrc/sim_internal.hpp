@@ -31,4 +31,11 @@ int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream);
 // take the call (several scales, output rows, tables beyond the LDS).
 int run_shared_stats(KArgs& a, int smax, hipStream_t stream);
 
+// Shared-trace simulation on the segment-speculative kernels (one lane per
+// job, the trace cut into segments simulated at once and reconciled);
+// AS_E_LIMITS without launching when a wavefront's state does not fit in LDS.
+int run_spec(KArgs& a, int smax, hipStream_t stream);
+// Whether a shared-trace call takes the segment-speculative kernels.
+bool want_spec(const KArgs& a, int smax);
+
 }  // namespace as_host

@@ -16,12 +16,23 @@ pytestmark = pytest.mark.gpu
 
 
 # kernel selections the library offers (environment variables read per call):
-# the shared-trace kernel (one group per lane), and the general LDS-staged
-# kernel with one or two groups per lane
+# the shared-trace kernel (one group per lane), the general LDS-staged kernel
+# with one or two groups per lane, and the segment-speculative kernels
 VARIANTS = {
-    "shared": {},
+    "shared": {"ALPASERVE_PATH": "shared"},
     "lds": {"ALPASERVE_PATH": "lds", "ALPASERVE_GPL": "1"},
     "lds_gpl2": {"ALPASERVE_PATH": "lds", "ALPASERVE_GPL": "2"},
+    # one lane per job over trace segments run at once and reconciled: the
+    # default segment count, an odd count, and 64 segments (short and empty
+    # segments whose states never meet: many reconciliation rounds)
+    "spec": {"ALPASERVE_PATH": "spec"},
+    "spec_seg7": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "7"},
+    "spec_seg64": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "64"},
+    # no warm-up: every segment starts from the empty state
+    "spec_seg7_cold": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "7", "ALPASERVE_SPEC_WARMUP": "0"},
+    # a warm-up shorter than a segment
+    "spec_seg16_warm100": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "16",
+                           "ALPASERVE_SPEC_WARMUP": "100"},
 }
 
 
@@ -37,7 +48,7 @@ def gpu_api():
 
 @pytest.fixture(params=sorted(VARIANTS))
 def gpu(request, gpu_api, monkeypatch):
-    for k in ("ALPASERVE_PATH", "ALPASERVE_GPL"):
+    for k in ("ALPASERVE_PATH", "ALPASERVE_GPL", "ALPASERVE_SPEC_SEGMENTS", "ALPASERVE_SPEC_WARMUP"):
         monkeypatch.delenv(k, raising=False)
     for k, v in VARIANTS[request.param].items():
         monkeypatch.setenv(k, v)
@@ -233,6 +244,30 @@ def test_c4_full_size_sampled(gpu_api):
                                                                            int(pb.finish_jobs[-1])})
     fins = [int(pb.finish_jobs[0]), int(pb.finish_jobs[-1])]
     compare(res, oracle_problem(pb, jobs=jobs, finish_jobs=fins), len(pb.t), "c4 full sampled")
+
+
+def test_c4_full_size_spec_sampled(gpu_api, monkeypatch):
+    """The benchmark workload at full size on the segment-speculative kernels
+    (default segment count): oracle samples as above, and every job's served
+    count and digest equal to those of the shared-trace kernel (itself checked
+    against the oracle in the test above)."""
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c4_heavy()
+    monkeypatch.setenv("ALPASERVE_PATH", "spec")
+    say("c4 full spec", pb.n_jobs, len(pb.t))
+    res = gpu_api.simulate_problem(pb)
+    rng = np.random.default_rng(45)
+    jobs = sorted(set(rng.choice(pb.n_jobs, 6, replace=False).tolist()) | {int(pb.finish_jobs[0]),
+                                                                           int(pb.finish_jobs[-1])})
+    fins = [int(pb.finish_jobs[0]), int(pb.finish_jobs[-1])]
+    compare(res, oracle_problem(pb, jobs=jobs, finish_jobs=fins), len(pb.t), "c4 full spec sampled")
+    monkeypatch.setenv("ALPASERVE_PATH", "shared")
+    ref = gpu_api.simulate_problem(pb)
+    assert np.array_equal(res["served"], ref["served"])
+    assert np.array_equal(np.asarray(res["digest"]), np.asarray(ref["digest"]))
+    for f in range(len(pb.finish_jobs)):
+        j = int(pb.finish_jobs[f])
+        assert res["finish"][j].tobytes() == ref["finish"][j].tobytes(), j
 
 
 def test_maximum_sizes(gpu):
