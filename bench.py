@@ -49,7 +49,7 @@ HBM_PEAK = 8.0e12
 # change, traffic is reported as null until it is measured again.
 KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd/csrc/sim_kernel.hpp",
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
-                  "paper_2302_11665_amd/csrc/sim_shared.hpp"]
+                  "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
     "sources_sha256": "ddf7a7ceaf5e9fd6bbc28c9b7ec050104e1fe2d5c98dcfbed6002dfb63876eec",
     "kernel": "shared_kernel<16, 4, true, false>",

@@ -152,20 +152,28 @@ bool choose_shape(int G, int64_t J, bool seg, int M, int C, int smax, int& W, in
   return found;
 }
 
-// Which kernel family runs a shared-trace call: the scalar path by default;
-// ALPASERVE_PATH=lds selects the LDS-staged kernel, =spec the
-// segment-speculative one, =shared the shared-trace one (tests cover each).
+// Which kernel family runs a shared-trace call: by default the
+// segment-speculative kernels when the trace splits into segments, else the
+// shared-trace kernel; ALPASERVE_PATH=lds selects the LDS-staged kernel,
+// =spec the segment-speculative one, =shared the shared-trace one (tests
+// cover each).
 bool use_shared_path() {
   const char* e = getenv("ALPASERVE_PATH");
   return !(e && std::strcmp(e, "lds") == 0);
 }
 
+// The segment-speculative kernels take a call unless another family is
+// forced; they decline (AS_E_LIMITS) calls they cannot cut into segments.
 bool want_spec(const KArgs& a, int smax) {
+  (void)a;
   (void)smax;
   const char* e = getenv("ALPASERVE_PATH");
-  if (e && *e) return std::strcmp(e, "spec") == 0;
-  (void)a;
-  return false;
+  return !(e && *e) || std::strcmp(e, "spec") == 0;
+}
+
+bool spec_forced() {
+  const char* e = getenv("ALPASERVE_PATH");
+  return e && std::strcmp(e, "spec") == 0;
 }
 
 // Checks shared by both simulate entry points; fills the model/placement part

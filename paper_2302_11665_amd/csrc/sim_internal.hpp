@@ -37,5 +37,7 @@ int run_shared_stats(KArgs& a, int smax, hipStream_t stream);
 int run_spec(KArgs& a, int smax, hipStream_t stream);
 // Whether a shared-trace call takes the segment-speculative kernels.
 bool want_spec(const KArgs& a, int smax);
+// Whether ALPASERVE_PATH=spec forces them (even with a single segment).
+bool spec_forced();
 
 }  // namespace as_host

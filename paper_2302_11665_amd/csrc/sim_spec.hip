@@ -14,9 +14,10 @@
 //            (all F = 0), then runs the segment from that estimate,
 //            recording its results and the state at its end;
 //   round q  segment k whose recorded start state differs from the end state
-//            segment k-1 now has re-runs its requests from that end state and,
-//            in lockstep, from its old start state, until the two states are
-//            equal bit for bit: from there on both runs take identical
+//            segment k-1 now has re-runs its requests from that end state
+//            until its state equals, bit for bit, the state its current
+//            results had at the same request (pass 0 saves the state every
+//            few thousand requests): from there on both runs take identical
 //            decisions (the state is the only thing a request depends on
 //            besides its own arrival), so the old results stand and only the
 //            re-run prefix is replaced.  A segment whose runs never meet gets
@@ -40,6 +41,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <type_traits>
@@ -73,6 +75,11 @@ struct SpecArgs {
   double* st_end;       // [2][nseg][G*SMAX][J] end states, alternating between rounds
   int64_t* seg_served;  // [nseg][J]
   uint64_t* seg_fsum;   // [nseg][J]
+  double* ckpt;         // [nseg][ckps][G*SMAX][J] states every ck requests into a segment
+  int64_t* ck_served;   // [nseg][ckps][J] served count of the segment before each checkpoint
+  uint64_t* ck_fsum;    // [nseg][ckps][J] finish-time sum likewise
+  int64_t ck;           // checkpoint interval (a multiple of 64)
+  int32_t ckps;         // checkpoints per segment (upper bound)
   int32_t* changed;     // [nseg] segments whose end state changed, per round
   int32_t* cfg_info;    // [2]: 1 when every used group has one configuration; that configuration
   int64_t nw;
@@ -90,84 +97,71 @@ __device__ __forceinline__ uint64_t bits_of(double x) { return (uint64_t)__doubl
 
 // Hosting masks of one lane's placement for every model, MB bits per model,
 // held in vector registers (32-dword vector values: a wavefront-uniform index
-// into one lowers to indexed register moves, not memory).  With at most 16
-// groups each model also has a host list: its lowest eight hosting groups as
-// 4-bit fields in increasing order, unused fields repeating the lowest host.
+// into one lowers to indexed register moves, not memory).
 typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
-
-// Element m (wavefront-uniform, < 64) of the 64-dword pair (x0, x1): one
-// indexed register move per half, then a select of the two dwords (the empty
-// asm keeps the compiler from selecting whole vectors first).
-__device__ __forceinline__ uint32_t pick2(const u32x32& x0, const u32x32& x1, int m) {
-  uint32_t a = x0[m & 31], b = x1[m & 31];
-  asm volatile("" : "+v"(a), "+v"(b));
-  return m < 32 ? a : b;
-}
 
 template <int MB>
 struct LaneMasks {
-  using MaskT = typename std::conditional<MB <= 32, uint32_t, uint64_t>::type;
-  static constexpr int kVecs = 64 * MB / 32 / 32;  // 1, 2 or 4
-  static constexpr int kListVecs = MB == 16 ? 2 : 0;
-  u32x32 v[kVecs];
-  u32x32 hl[kListVecs > 0 ? kListVecs : 1];
+  static_assert(MB == 32 || MB == 64, "32- or 64-bit hosting masks");
+  using MaskT = typename std::conditional<MB == 32, uint32_t, uint64_t>::type;
+  // named vectors, never an array of them: a variable first index would put
+  // the registers in memory.  MB 32 uses v0-v1, MB 64 v0-v3.
+  u32x32 v0, v1, v2, v3;
+  __device__ __forceinline__ void put(int w, uint32_t x) {  // dword w of the masks
+    if (w < 32) {
+      v0[w & 31] = x;
+    } else if (w < 64) {
+      v1[w & 31] = x;
+    } else if constexpr (MB == 64) {
+      if (w < 96) {
+        v2[w & 31] = x;
+      } else {
+        v3[w & 31] = x;
+      }
+    }
+  }
   // bits of groups >= G are dropped (they name no state)
   __device__ __forceinline__ void load(const uint64_t* row, int M, int G, bool valid) {
-#pragma unroll
-    for (int q = 0; q < kVecs; ++q) v[q] = (u32x32)(0u);
-#pragma unroll
-    for (int q = 0; q < (kListVecs > 0 ? kListVecs : 1); ++q) hl[q] = (u32x32)(0u);
+    v0 = v1 = (u32x32)(0u);
+    if constexpr (MB == 64) v2 = v3 = (u32x32)(0u);
     if (!valid) return;
     const uint64_t keep = G >= 64 ? ~0ull : (1ull << G) - 1;
 #pragma unroll
     for (int m = 0; m < 64; ++m) {
       const uint64_t x = m < M ? row[m] & keep : 0;
-      if constexpr (MB == 16) {
-        v[0][m >> 1] |= (uint32_t)(x & 0xFFFFu) << ((m & 1) * 16);
-        uint32_t rest = (uint32_t)x, list = 0;
-        const uint32_t low = rest ? (uint32_t)__builtin_ctz(rest) : 0u;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const uint32_t h = rest ? (uint32_t)__builtin_ctz(rest) : low;
-          rest &= rest - 1;
-          list |= h << (4 * q);
-        }
-        hl[m >> 5][m & 31] = list;
-      } else if constexpr (MB == 32) {
-        v[m >> 5][m & 31] = (uint32_t)x;
+      if constexpr (MB == 32) {
+        put(m, (uint32_t)x);
       } else {
-        v[m >> 4][(2 * m) & 31] = (uint32_t)x;
-        v[m >> 4][(2 * m + 1) & 31] = (uint32_t)(x >> 32);
+        put(2 * m, (uint32_t)x);
+        put(2 * m + 1, (uint32_t)(x >> 32));
       }
     }
   }
-  // m is wavefront-uniform
+  // m is wavefront-uniform; one indexed register move per vector read (the
+  // empty asm keeps the compiler from selecting whole vectors first)
   __device__ __forceinline__ MaskT get(int m) const {
-    if constexpr (MB == 16) {
-      return (v[0][m >> 1] >> ((m & 1) * 16)) & 0xFFFFu;
-    } else if constexpr (MB == 32) {
-      return pick2(v[0], v[1], m);
+    if constexpr (MB == 32) {
+      uint32_t lo = v0[m & 31], hi = v1[m & 31];
+      asm volatile("" : "+v"(lo), "+v"(hi));
+      return m < 32 ? lo : hi;
     } else {
-      const int q = m >> 4, e = (2 * m) & 31;
-      uint32_t lo = v[0][e], hi = v[0][e + 1];
-      if (q == 1) {
-        lo = v[1][e];
-        hi = v[1][e + 1];
-      } else if (q == 2) {
-        lo = v[2][e];
-        hi = v[2][e + 1];
-      } else if (q == 3) {
-        lo = v[3][e];
-        hi = v[3][e + 1];
+      const int e = (2 * m) & 31;
+      uint32_t lo, hi;
+      if (m < 16) {
+        lo = v0[e];
+        hi = v0[e + 1];
+      } else if (m < 32) {
+        lo = v1[e];
+        hi = v1[e + 1];
+      } else if (m < 48) {
+        lo = v2[e];
+        hi = v2[e + 1];
+      } else {
+        lo = v3[e];
+        hi = v3[e + 1];
       }
+      asm volatile("" : "+v"(lo), "+v"(hi));
       return (uint64_t)lo | ((uint64_t)hi << 32);
-    }
-  }
-  __device__ __forceinline__ uint32_t list(int m) const {
-    if constexpr (MB == 16) {
-      return pick2(hl[0], hl[1], m);
-    } else {
-      return 0;
     }
   }
 };
@@ -181,18 +175,21 @@ __device__ __forceinline__ int ctz_any(T x) {
   }
 }
 
-// Per-wavefront LDS: the stage-latency table and per-lane group
-// configurations when groups differ, then one or two state regions.
+// Per-wavefront LDS: the model table, per-lane group configurations when
+// groups differ, then the state.
+//   uniform configuration c0:  T[m] = {L[m][c0][0..SMAX-1], d_single[m]}
+//   otherwise:                 L[m][c][0..SMAX-1], D[m] = d_single[m], cfg[g][lane]
 template <int SMAX, bool UCFG>
 struct SpecLds {
-  double* L;      // !UCFG: [M][C][SMAX]
+  double* T;      // UCFG: [M][SMAX + 1]; else L: [M][C][SMAX]
+  double* D;      // !UCFG: [M]
   uint16_t* cfg;  // !UCFG: [G][64] = c | S << 8
-  double* F0;     // [G][SMAX][64]
-  double* F1;     // second state (rounds)
+  double* F;      // [G][SMAX][64]
 };
 
-__host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg, int states) {
-  return (ucfg ? 0 : (size_t)M * C * SMAX * 8 + (size_t)G * 64 * 2) + (size_t)states * G * SMAX * 64 * 8;
+__host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg) {
+  return (ucfg ? (size_t)M * (SMAX + 1) * 8 : (size_t)M * C * SMAX * 8 + (size_t)M * 8 + (size_t)G * 64 * 2) +
+         (size_t)G * SMAX * 64 * 8;
 }
 
 __device__ __forceinline__ double readlane_f64(double v, int l) {
@@ -203,168 +200,180 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
 
 template <int SMAX, bool UCFG>
 __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, double* lds, int lane, int p,
-                                                           bool valid, int states) {
+                                                           bool valid, int c0) {
   SpecLds<SMAX, UCFG> s;
-  double* after = lds;
-  s.L = nullptr;
-  s.cfg = nullptr;
-  if constexpr (!UCFG) {
-    const int M = a.M, C = a.C;
-    s.L = lds;
-    s.cfg = reinterpret_cast<uint16_t*>(s.L + (size_t)M * C * SMAX);
-    after = reinterpret_cast<double*>(s.cfg + (size_t)a.G * 64);
+  const int M = a.M, C = a.C;
+  s.T = lds;
+  if constexpr (UCFG) {
+    s.D = nullptr;
+    s.cfg = nullptr;
+    s.F = s.T + (size_t)M * (SMAX + 1);
+    const int S0 = a.cfg_stages[c0];
+    for (int e = lane; e < M * (SMAX + 1); e += 64) {
+      const int k = e % (SMAX + 1);
+      const int m = e / (SMAX + 1);
+      s.T[e] = k == SMAX ? a.d_single[m]
+                         : (k < S0 ? a.stage_lat[((int64_t)m * C + c0) * a.smax_in + k] : 0.0);
+    }
+  } else {
+    s.D = s.T + (size_t)M * C * SMAX;
+    s.cfg = reinterpret_cast<uint16_t*>(s.D + M);
+    s.F = reinterpret_cast<double*>(s.cfg + (size_t)a.G * 64);
     // stage latencies (0 beyond S_c: never used)
     for (int e = lane; e < M * C * SMAX; e += 64) {
       const int k = e % SMAX;
       const int c = (e / SMAX) % C;
       const int m = e / (SMAX * C);
-      s.L[e] = k < a.cfg_stages[c] ? a.stage_lat[((int64_t)m * C + c) * a.smax_in + k] : 0.0;
+      s.T[e] = k < a.cfg_stages[c] ? a.stage_lat[((int64_t)m * C + c) * a.smax_in + k] : 0.0;
     }
+    for (int m = lane; m < M; m += 64) s.D[m] = a.d_single[m];
     for (int g = 0; g < a.G; ++g) {
       int c = valid ? a.group_cfg[(int64_t)p * a.G + g] : -1;
       if (c < 0 || c >= C) c = 0;  // a group hosting nothing is never chosen
       s.cfg[g * 64 + lane] = (uint16_t)(c | (a.cfg_stages[c] << 8));
     }
   }
-  s.F0 = after;
-  s.F1 = states > 1 ? s.F0 + (size_t)a.G * SMAX * 64 : nullptr;
   __syncthreads();
   return s;
 }
 
-// Uniform data of one request: arrival, model, its SLO base d_single[m] and
-// (uniform configuration) its stage latencies, the last two read with scalar
-// loads (the tables are read-only for the whole launch).
-template <int SMAX, bool UCFG>
-struct Req {
+// The wavefront-uniform part of a request and this lane's hosting groups:
+// arrival t, model m, hosting mask, the two lowest hosting groups (both the
+// lowest when there is one; 0 when there is none) and whether the lane has
+// more.
+template <int MB>
+struct Plan {
+  using MaskT = typename LaneMasks<MB>::MaskT;
   double t;
   int m;
+  MaskT mask;
+  int g0, g1;
+  bool more;
+};
+
+template <int MB>
+__device__ __forceinline__ Plan<MB> make_plan(const SpecArgs& a, const LaneMasks<MB>& msk, double t, int m) {
+  Plan<MB> pl;
+  pl.t = t;
+  pl.m = m;
+  const bool known = (unsigned)m < (unsigned)a.M;
+  pl.mask = known ? msk.get(m) : 0;
+  const auto r1 = pl.mask & (pl.mask - 1);
+  pl.g0 = pl.mask ? ctz_any(pl.mask) : 0;
+  pl.g1 = r1 ? ctz_any(r1) : pl.g0;
+  pl.more = (r1 & (r1 - 1)) != 0;
+  return pl;
+}
+
+// LDS reads of one request, issued together: the rows of the two lowest
+// hosting groups, the stage-0 entries of up to six more hosts when some lane
+// of the wavefront has them, and the model's table row.
+template <int SMAX, bool UCFG>
+struct Reads {
+  static constexpr int kX = 6;
+  double A[SMAX], B[SMAX], X[kX];
+  int hx[kX];
+  bool extra;
   double L[UCFG ? SMAX : 1];
   double d;
 };
 
-typedef const __attribute__((address_space(4))) double* const_f64_ptr;
-
-template <int SMAX, bool UCFG>
-__device__ __forceinline__ void req_tables(const SpecArgs& a, int c0, int S0, Req<SMAX, UCFG>& q) {
-  const int mi = (unsigned)q.m < (unsigned)a.M ? q.m : 0;
-  const const_f64_ptr dc = (const_f64_ptr)a.d_single;
-  q.d = dc[mi];
-  if constexpr (UCFG) {
-    // stages past S0 read stage 0 again (their result is never used)
-    const const_f64_ptr Lc = (const_f64_ptr)a.stage_lat;
-    const int base = (mi * a.C + c0) * a.smax_in;  // < 64 * 32 * 8
-#pragma unroll
-    for (int k = 0; k < SMAX; ++k) q.L[k] = Lc[base + (k < S0 ? k : 0)];
-  }
-}
-
-// One request of one lane on the state F: dispatch (least stage-0 free time
-// among the hosting groups, lowest index on ties), stage chain, admission
-// (finish <= t + scale * d_single[m]), commit.  Returns the finish time (-1
-// dropped, -2 no hosting group) and the chosen group in gs (-1 when nothing
-// was committed).  The LDS reads of a request go out together: the rows of
-// the two lowest hosting groups and, when some lane of the wavefront has
-// more hosts, the stage-0 entries of up to six more; a row is read again only
-// when one of those wins.
 template <int SMAX, bool UCFG, int MB>
-__device__ __forceinline__ double spec_step(const SpecLds<SMAX, UCFG>& s, double* F, int lane,
-                                            typename LaneMasks<MB>::MaskT mask, uint32_t hlist,
-                                            const Req<SMAX, UCFG>& r, double scale, int C, int S0, int& gs) {
-  using MaskT = typename LaneMasks<MB>::MaskT;
-  constexpr int kX = 6;
-  gs = -1;
-  if (mask == 0) return -2.0;
-  int g0, g1;
-  MaskT rest;  // hosts after the eighth (host lists) or after the second
-  bool more;   // this lane has a third host
-  int hx[kX];
-  if constexpr (MB == 16) {
-    g0 = (int)(hlist & 15u);
-    g1 = (int)((hlist >> 4) & 15u);
-    const int cnt = __builtin_popcount((uint32_t)mask);
-    more = cnt > 2;
-#pragma unroll
-    for (int q = 0; q < kX; ++q) hx[q] = (int)((hlist >> (4 * (q + 2))) & 15u);
-    rest = 0;
-    if (cnt > 8) {
-      rest = mask;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) rest &= rest - 1;
-    }
-  } else {
-    g0 = ctz_any(mask);
-    const MaskT r1 = mask & (mask - 1);
-    g1 = r1 ? ctz_any(r1) : g0;
-    rest = r1 & (r1 - 1);
-    more = rest != 0;
-  }
-  const bool extra = __builtin_amdgcn_ballot_w64(more) != 0;
-  if constexpr (MB != 16) {
-    if (extra) {
-#pragma unroll
-      for (int q = 0; q < kX; ++q) {
-        hx[q] = rest ? ctz_any(rest) : g0;
-        rest &= rest - 1;
-      }
-    }
-  }
-  double A[SMAX], B[SMAX], X[kX];
+__device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
+                                                         int lane) {
+  constexpr int kX = Reads<SMAX, UCFG>::kX;
+  Reads<SMAX, UCFG> rd;
 #pragma unroll
   for (int k = 0; k < SMAX; ++k) {
-    A[k] = F[(g0 * SMAX + k) * 64 + lane];
-    B[k] = F[(g1 * SMAX + k) * 64 + lane];
+    rd.A[k] = s.F[(pl.g0 * SMAX + k) * 64 + lane];
+    rd.B[k] = s.F[(pl.g1 * SMAX + k) * 64 + lane];
   }
-  if (extra) {
+  rd.extra = __builtin_amdgcn_ballot_w64(pl.more) != 0;
+  if (rd.extra) {
+    auto rest = pl.mask & (pl.mask - 1);
+    rest &= rest - 1;
 #pragma unroll
-    for (int q = 0; q < kX; ++q) X[q] = F[(hx[q] * SMAX) * 64 + lane];
+    for (int q = 0; q < kX; ++q) {
+      rd.hx[q] = rest ? ctz_any(rest) : pl.g0;
+      rest &= rest - 1;
+    }
+#pragma unroll
+    for (int q = 0; q < kX; ++q) rd.X[q] = s.F[(rd.hx[q] * SMAX) * 64 + lane];
   }
+  const int mi = (unsigned)pl.m < 64u ? pl.m : 0;
+  if constexpr (UCFG) {
+    const double* row = s.T + mi * (SMAX + 1);
+#pragma unroll
+    for (int k = 0; k < SMAX; ++k) rd.L[k] = row[k];
+    rd.d = row[SMAX];
+  } else {
+    rd.d = s.D[mi];
+  }
+  return rd;
+}
+
+// Dispatch (least stage-0 free time among the hosting groups, lowest index on
+// ties), stage chain, admission (finish <= t + scale * d_single[m]) and
+// commit of one request on the lane's state.  Returns the finish time (-1
+// dropped, -2 no hosting group); gs is the group committed to, -1 if none.
+template <int SMAX, bool UCFG, int MB>
+__device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
+                                              const Reads<SMAX, UCFG>& rd, int lane, double scale, int C, int S0,
+                                              int& gs) {
+  constexpr int kX = Reads<SMAX, UCFG>::kX;
   // g1 > g0, and further hosts come in increasing order: strict comparisons
   // keep the lowest index among equal free times
-  const bool use_b = B[0] < A[0];
-  int g = use_b ? g1 : g0;
+  const bool use_b = rd.B[0] < rd.A[0];
+  int g = use_b ? pl.g1 : pl.g0;
   double Fv[SMAX];
 #pragma unroll
-  for (int k = 0; k < SMAX; ++k) Fv[k] = use_b ? B[k] : A[k];
-  if (extra) {
+  for (int k = 0; k < SMAX; ++k) Fv[k] = use_b ? rd.B[k] : rd.A[k];
+  if (rd.extra) {
     double best = Fv[0];
 #pragma unroll
     for (int q = 0; q < kX; ++q) {
-      if (X[q] < best) {
-        best = X[q];
-        g = hx[q];
+      if (rd.X[q] < best) {
+        best = rd.X[q];
+        g = rd.hx[q];
       }
     }
-    while (rest) {  // more than eight hosts
-      const int h = ctz_any(rest);
-      rest &= rest - 1;
-      const double v = F[(h * SMAX) * 64 + lane];
-      if (v < best) {
-        best = v;
-        g = h;
-      }
-    }
-    if (g != g0 && g != g1) {
+    // hosts after the eighth
+    typename LaneMasks<MB>::MaskT rest = pl.mask;
+    if (__popcll((uint64_t)pl.mask) > 8) {
 #pragma unroll
-      for (int k = 0; k < SMAX; ++k) Fv[k] = F[(g * SMAX + k) * 64 + lane];
+      for (int q = 0; q < 8; ++q) rest &= rest - 1;
+      while (rest) {
+        const int h = ctz_any(rest);
+        rest &= rest - 1;
+        const double v = s.F[(h * SMAX) * 64 + lane];
+        if (v < best) {
+          best = v;
+          g = h;
+        }
+      }
+    }
+    if (g != pl.g0 && g != pl.g1) {
+#pragma unroll
+      for (int k = 0; k < SMAX; ++k) Fv[k] = s.F[(g * SMAX + k) * 64 + lane];
     }
   }
   double Lv[SMAX];
   int S = S0;
   if constexpr (UCFG) {
 #pragma unroll
-    for (int k = 0; k < SMAX; ++k) Lv[k] = r.L[k];
+    for (int k = 0; k < SMAX; ++k) Lv[k] = rd.L[k];
   } else {
     const uint32_t e = s.cfg[g * 64 + lane];
     const int c = (int)(e & 0xFF);
     S = (int)(e >> 8);
-    const double* Lrow = s.L + ((size_t)r.m * C + c) * SMAX;
+    const int mi = (unsigned)pl.m < 64u ? pl.m : 0;
+    const double* Lrow = s.T + ((size_t)mi * C + c) * SMAX;
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) Lv[k] = Lrow[k];
   }
   // projection through the stage chain; stages past S keep their state
   double f[SMAX];
-  double prev = r.t;
+  double prev = pl.t;
   if (UCFG && S == SMAX) {
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) {
@@ -380,11 +389,13 @@ __device__ __forceinline__ double spec_step(const SpecLds<SMAX, UCFG>& s, double
       prev = in ? x : prev;
     }
   }
-  const double slo = scale * r.d;
-  const double deadline = r.t + slo;
+  const double slo = scale * rd.d;
+  const double deadline = pl.t + slo;
+  gs = -1;
+  if (pl.mask == 0) return -2.0;
   if (prev > deadline) return -1.0;
 #pragma unroll
-  for (int k = 0; k < SMAX; ++k) F[(g * SMAX + k) * 64 + lane] = f[k];
+  for (int k = 0; k < SMAX; ++k) s.F[(g * SMAX + k) * 64 + lane] = f[k];
   gs = g;
   return prev;
 }
@@ -408,34 +419,78 @@ __device__ __forceinline__ SpecLane spec_lane(const SpecArgs& a, int jb, int lan
   return l;
 }
 
-// Arrivals in chunks of 64 (lane r holds request base + r); the next chunk is
-// loaded while the current one is simulated.
+// Arrivals of [from, to) in chunks of 64 (lane r holds request base + r),
+// the next chunk loaded while the current one is simulated.
 struct TraceChunks {
   double tv, tn;
   int mv, mn;
-  __device__ __forceinline__ void first(const SpecArgs& a, int64_t b, int64_t e, int lane) {
-    const int64_t i = b + lane;
-    tn = i < e ? a.t[i] : 0.0;
-    mn = i < e ? a.model[i] : 0;
+  int64_t to;
+  __device__ __forceinline__ void first(const SpecArgs& a, int64_t from, int64_t to_, int lane) {
+    to = to_;
+    const int64_t i = from + lane;
+    tn = i < to ? a.t[i] : 0.0;
+    mn = i < to ? a.model[i] : 0;
   }
-  __device__ __forceinline__ void advance(const SpecArgs& a, int64_t next_base, int64_t e, int lane) {
+  __device__ __forceinline__ void advance(const SpecArgs& a, int64_t next_base, int lane) {
     tv = tn;
     mv = mn;
     const int64_t i = next_base + lane;
-    tn = i < e ? a.t[i] : 0.0;
-    mn = i < e ? a.model[i] : 0;
-  }
-  template <int SMAX, bool UCFG>
-  __device__ __forceinline__ Req<SMAX, UCFG> get(const SpecArgs& a, int r, int c0, int S0) const {
-    Req<SMAX, UCFG> q;
-    q.t = readlane_f64(tv, r);
-    q.m = __builtin_amdgcn_readlane(mv, r);
-    req_tables<SMAX, UCFG>(a, c0, S0, q);
-    return q;
+    tn = i < to ? a.t[i] : 0.0;
+    mn = i < to ? a.model[i] : 0;
   }
 };
 
-// Pass 0: every (job, segment) from the empty state.
+// Simulate requests [from, to) of one lane (only while the lane is active)
+// with the next request's preparation overlapping the current one's LDS
+// reads.  Per chunk of 64 requests: chunk_begin(base) may stop the loop
+// (returns false once no lane of the wavefront is active), result(i, r, out,
+// gs) sees every simulated request, chunk_end(base, cnt) closes the chunk.
+template <int SMAX, int MB, bool UCFG, class Begin, class Result, class End>
+__device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
+                                           const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int S0,
+                                           int64_t from, int64_t to, const bool& active, Begin chunk_begin,
+                                           Result result, End chunk_end) {
+  if (from >= to) return;
+  TraceChunks tc;
+  tc.first(a, from, to, lane);
+  tc.advance(a, from + 64, lane);
+  Plan<MB> cur = make_plan<MB>(a, msk, readlane_f64(tc.tv, 0), __builtin_amdgcn_readlane(tc.mv, 0));
+  for (int64_t cb = from; cb < to; cb += 64) {
+    if (!chunk_begin(cb)) return;
+    const int cnt = (int)(to - cb < 64 ? to - cb : 64);
+    const bool last_chunk = cb + 64 >= to;
+    for (int r = 0; r < cnt; ++r) {
+      Reads<SMAX, UCFG> rd;
+      if (active) rd = issue_reads<SMAX, UCFG, MB>(s, cur, lane);
+      // the next request (the next chunk's first at the end of a chunk; past
+      // the range a placeholder), prepared while this one's reads are in
+      // flight
+      double t_nx;
+      int m_nx;
+      if (r + 1 < cnt) {
+        t_nx = readlane_f64(tc.tv, r + 1);
+        m_nx = __builtin_amdgcn_readlane(tc.mv, r + 1);
+      } else {
+        t_nx = readlane_f64(tc.tn, 0);
+        m_nx = __builtin_amdgcn_readlane(tc.mn, 0);
+      }
+      const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, m_nx);
+      if (active) {
+        int gs;
+        const double out = finish_step<SMAX, UCFG, MB>(s, cur, rd, lane, ln.scale, a.C, S0, gs);
+        result(cb + r, r, out, gs);
+      }
+      cur = nxt;
+    }
+    chunk_end(cb, cnt);
+    if (!last_chunk) tc.advance(a, cb + 128, lane);
+  }
+}
+
+__device__ __forceinline__ int spec_ckpts(int64_t b, int64_t e, int64_t ck) { return (int)((e - b - 1) / ck); }
+
+// Pass 0: every (job, segment) from a warmed-up estimate of its start state;
+// the state is also saved every ck requests (checkpoints for the rounds).
 template <int SMAX, int MB, bool UCFG>
 __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   // both variants are launched; the one that does not match the placements
@@ -449,70 +504,68 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const SpecLane ln = spec_lane(a, jb, lane);
   LaneMasks<MB> msk;
   msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-  const auto s = spec_tables<SMAX, UCFG>(a, lds, lane, ln.p, ln.valid, 1);
+  const auto s = spec_tables<SMAX, UCFG>(a, lds, lane, ln.p, ln.valid, c0);
   const int GS = a.G * SMAX;
-  for (int q = 0; q < GS; ++q) s.F0[q * 64 + lane] = 0.0;
+  for (int q = 0; q < GS; ++q) s.F[q * 64 + lane] = 0.0;
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
-  const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
   if (blockIdx.x == 0 && lane < a.nseg) a.changed[lane] = lane == 0 ? 1 : 0;
+  const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
 
   const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
   const int64_t J = a.J;
+  const bool on = true;
   // warm-up: the requests just before the segment, from the empty state, give
   // its start state (usually already the exact one: the rounds then find
-  // nothing to redo)
-  const int64_t w0 = b > a.warmup ? b - a.warmup : 0;
-  if (k > 0 && w0 < b) {
-    TraceChunks tw;
-    tw.first(a, w0, b, lane);
-    for (int64_t cb = w0; cb < b; cb += 64) {
-      tw.advance(a, cb + 64, b, lane);
-      const int cnt = (int)(b - cb < 64 ? b - cb : 64);
-      for (int r = 0; r < cnt; ++r) {
-        const Req<SMAX, UCFG> rq = tw.template get<SMAX, UCFG>(a, r, c0, S0);
-        const bool known = (unsigned)rq.m < (unsigned)a.M;
-        const typename LaneMasks<MB>::MaskT mask = known ? msk.get(rq.m) : 0;
-        const uint32_t hl = known ? msk.list(rq.m) : 0u;
-        int gs;
-        (void)spec_step<SMAX, UCFG, MB>(s, s.F0, lane, mask, hl, rq, ln.scale, a.C, S0, gs);
-      }
-    }
-  }
+  // nothing to redo); one pass over [w0, e) records from b on
+  const int64_t wu = (a.warmup + 63) & ~(int64_t)63;
+  const int64_t w0 = k == 0 ? b : (b > wu ? b - wu : 0);
   const size_t seg_base = ((size_t)k * GS) * J + ln.job;
-  if (ln.valid)
-    for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F0[q * 64 + lane];
   int64_t served = 0;
-  uint64_t fsum = 0;
-  TraceChunks tc;
-  tc.first(a, b, e, lane);
-  for (int64_t cb = b; cb < e; cb += 64) {
-    tc.advance(a, cb + 64, e, lane);
-    const int cnt = (int)(e - cb < 64 ? e - cb : 64);
-    uint64_t word = 0;
-    for (int r = 0; r < cnt; ++r) {
-      const Req<SMAX, UCFG> rq = tc.template get<SMAX, UCFG>(a, r, c0, S0);
-      int gs;
-      const bool known = (unsigned)rq.m < (unsigned)a.M;
-        const typename LaneMasks<MB>::MaskT mask = known ? msk.get(rq.m) : 0;
-        const uint32_t hl = known ? msk.list(rq.m) : 0u;
-      const double out = spec_step<SMAX, UCFG, MB>(s, s.F0, lane, mask, hl, rq, ln.scale, a.C, S0, gs);
-      if (gs >= 0) {
-        served += 1;
-        fsum += bits_of(out);
-        word |= 1ull << r;
-      }
-      if (wave_rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + cb + r] = out;
-    }
-    if (ln.valid) a.bitmap[(cb >> 6) * J + ln.job] = word;
-  }
+  uint64_t fsum = 0, word = 0;
+  const size_t ck0 = (size_t)k * a.ckps;
+  if (w0 == b && ln.valid)
+    for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
+  spec_range<SMAX, MB, UCFG>(
+      a, s, msk, ln, lane, S0, w0, e, on,
+      [&](int64_t cb) {
+        if (cb == b && w0 < b && ln.valid)
+          for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * 64 + lane];
+        if (cb > b && (cb - b) % a.ck == 0 && ln.valid) {
+          const size_t j = ck0 + (size_t)((cb - b) / a.ck - 1);
+          for (int q = 0; q < GS; ++q) a.ckpt[(j * GS + q) * J + ln.job] = s.F[q * 64 + lane];
+          a.ck_served[j * J + ln.job] = served;
+          a.ck_fsum[j * J + ln.job] = fsum;
+        }
+        return true;
+      },
+      [&](int64_t i, int r, double out, int gs) {
+        if (i < b) return;
+        if (gs >= 0) {
+          served += 1;
+          fsum += bits_of(out);
+          word |= 1ull << r;
+        }
+        if (wave_rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+      },
+      [&](int64_t cb, int) {
+        if (cb >= b && ln.valid) a.bitmap[(cb >> 6) * J + ln.job] = word;
+        word = 0;
+      });
+  // an empty segment's start state is its warm-up end
+  if (b == e && w0 < b && ln.valid)
+    for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * 64 + lane];
   if (!ln.valid) return;
-  for (int q = 0; q < GS; ++q) a.st_end[seg_base + (size_t)q * J] = s.F0[q * 64 + lane];  // buffer 0
+  for (int q = 0; q < GS; ++q) a.st_end[seg_base + (size_t)q * J] = s.F[q * 64 + lane];  // buffer 0
   a.seg_served[(size_t)k * J + ln.job] = served;
   a.seg_fsum[(size_t)k * J + ln.job] = fsum;
 }
 
-// Round q >= 1: segments whose start state is stale re-run in lockstep with
-// their old start until the two states meet.
+// Round q >= 1: a segment whose start state differs from its predecessor's
+// end state re-runs from that end state, comparing its state with the saved
+// checkpoints of its current results: where they are equal the two runs
+// coincide from there on, so the re-run stops and only its prefix replaces
+// the old results.  Checkpoints passed before that point are replaced with
+// the new run's.
 template <int SMAX, int MB, bool UCFG>
 __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   if ((a.cfg_info[0] != 0) != UCFG) return;
@@ -531,8 +584,6 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   const size_t own = ((size_t)k * GS) * J + ln.job;
   const size_t prv = k > 0 ? ((size_t)(k - 1) * GS) * J + ln.job : 0;
 
-  // the start state behind this segment's results versus the end state of
-  // its predecessor
   bool active = false;
   if (ln.valid && k > 0)
     for (int x = 0; x < GS; ++x)
@@ -545,86 +596,79 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   }
   LaneMasks<MB> msk;
   msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-  const auto s = spec_tables<SMAX, UCFG>(a, lds, lane, ln.p, ln.valid, 2);
+  const auto s = spec_tables<SMAX, UCFG>(a, lds, lane, ln.p, ln.valid, c0);
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
-  // F0: old run (from the stale start), F1: new run (from the predecessor's end)
-  uint64_t diff = 0;  // groups whose states differ
-  for (int x = 0; x < GS; ++x) {
-    const double o = active ? a.st_start[own + (size_t)x * J] : 0.0;
-    const double nv = active ? E_in[prv + (size_t)x * J] : 0.0;
-    s.F0[x * 64 + lane] = o;
-    s.F1[x * 64 + lane] = nv;
-    if (bits_of(o) != bits_of(nv)) diff |= 1ull << (x / SMAX);
-  }
+  for (int x = 0; x < GS; ++x) s.F[x * 64 + lane] = active ? E_in[prv + (size_t)x * J] : 0.0;
+
   const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
-  int64_t d_served = 0;
-  uint64_t d_fsum = 0;
+  const size_t ck0 = (size_t)k * a.ckps;
+  const int nck = b < e ? spec_ckpts(b, e, a.ck) : 0;
+  int64_t served = 0;
+  uint64_t fsum = 0, word = 0;
   bool coupled = false;
-  TraceChunks tc;
-  tc.first(a, b, e, lane);
-  for (int64_t cb = b; cb < e; cb += 64) {
-    if (__builtin_amdgcn_ballot_w64(active) == 0) break;
-    tc.advance(a, cb + 64, e, lane);
-    const int cnt = (int)(e - cb < 64 ? e - cb : 64);
-    uint64_t word = 0;
-    const bool part = active;  // this lane re-runs (part of) this chunk
-    int stop = cnt;            // its first request left to the old run
-    for (int r = 0; r < cnt; ++r) {
-      if (__builtin_amdgcn_ballot_w64(active) == 0) break;
-      const Req<SMAX, UCFG> rq = tc.template get<SMAX, UCFG>(a, r, c0, S0);
-      if (active) {
-        const bool known = (unsigned)rq.m < (unsigned)a.M;
-        const typename LaneMasks<MB>::MaskT mask = known ? msk.get(rq.m) : 0;
-        const uint32_t hl = known ? msk.list(rq.m) : 0u;
-        int go, gn;
-        const double oo = spec_step<SMAX, UCFG, MB>(s, s.F0, lane, mask, hl, rq, ln.scale, a.C, S0, go);
-        const double on = spec_step<SMAX, UCFG, MB>(s, s.F1, lane, mask, hl, rq, ln.scale, a.C, S0, gn);
-        d_served += (gn >= 0) - (go >= 0);
-        d_fsum += (gn >= 0 ? bits_of(on) : 0) - (go >= 0 ? bits_of(oo) : 0);
-        if (gn >= 0) word |= 1ull << r;
-        if (wave_rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + cb + r] = on;
-        // refresh the difference bits of the groups the two runs touched
-#pragma unroll
-        for (int w = 0; w < 2; ++w) {
-          const int g = w == 0 ? go : gn;
-          if (g < 0) continue;
+  spec_range<SMAX, MB, UCFG>(
+      a, s, msk, ln, lane, S0, b, e, active,
+      [&](int64_t cb) {
+        if (cb > b && (cb - b) % a.ck == 0 && active) {
+          const int jl = (int)((cb - b) / a.ck) - 1;
+          const size_t j = ck0 + (size_t)jl;
           bool same = true;
-#pragma unroll
-          for (int st = 0; st < SMAX; ++st)
-            same &= bits_of(s.F0[(g * SMAX + st) * 64 + lane]) == bits_of(s.F1[(g * SMAX + st) * 64 + lane]);
-          diff = same ? diff & ~(1ull << g) : diff | (1ull << g);
+          for (int x = 0; x < GS; ++x)
+            same &= bits_of(a.ckpt[(j * GS + x) * J + ln.job]) == bits_of(s.F[x * 64 + lane]);
+          const int64_t old_s = a.ck_served[j * J + ln.job];
+          const uint64_t old_f = a.ck_fsum[j * J + ln.job];
+          if (same) {
+            // the old results stand from here on; later checkpoints' running
+            // totals shift by the prefix's change
+            coupled = true;
+            active = false;
+            const int64_t ds = served - old_s;
+            const uint64_t df = fsum - old_f;
+            a.seg_served[(size_t)k * J + ln.job] += ds;
+            a.seg_fsum[(size_t)k * J + ln.job] += df;
+            a.ck_served[j * J + ln.job] = served;
+            a.ck_fsum[j * J + ln.job] = fsum;
+            for (int j2 = jl + 1; j2 < nck; ++j2) {
+              a.ck_served[(ck0 + j2) * J + ln.job] += ds;
+              a.ck_fsum[(ck0 + j2) * J + ln.job] += df;
+            }
+          } else {
+            for (int x = 0; x < GS; ++x) a.ckpt[(j * GS + x) * J + ln.job] = s.F[x * 64 + lane];
+            a.ck_served[j * J + ln.job] = served;
+            a.ck_fsum[j * J + ln.job] = fsum;
+          }
         }
-        if (diff == 0) {
-          coupled = true;
-          active = false;
-          stop = r + 1;
+        return __builtin_amdgcn_ballot_w64(active) != 0;
+      },
+      [&](int64_t i, int r, double out, int gs) {
+        if (gs >= 0) {
+          served += 1;
+          fsum += bits_of(out);
+          word |= 1ull << r;
         }
-      }
-    }
-    // accept bits of this chunk: the new run's before the lane's stop, the
-    // old run's (already stored) from there on
-    if (part) {
-      uint64_t* wp = a.bitmap + (cb >> 6) * J + ln.job;
-      if (stop >= cnt) {
-        *wp = word;
-      } else {
-        const uint64_t low = (1ull << stop) - 1;
-        *wp = (*wp & ~low) | word;
-      }
-    }
-  }
+        if (wave_rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+      },
+      [&](int64_t cb, int) {
+        if (active) a.bitmap[(cb >> 6) * J + ln.job] = word;
+        word = 0;
+      });
   if (!ln.valid) return;
   if (ran) {
     // the predecessor's end state now stands behind this segment's results
     for (int x = 0; x < GS; ++x) a.st_start[own + (size_t)x * J] = E_in[prv + (size_t)x * J];
-    a.seg_served[(size_t)k * J + ln.job] += d_served;
-    a.seg_fsum[(size_t)k * J + ln.job] += d_fsum;
     if (!coupled) {
-      // the runs never met: the segment ends in the new run's state
-      for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = s.F1[x * 64 + lane];
-      atomicAdd(a.changed + q, 1);
-      return;
+      // re-run to the end: its totals replace the old ones, and unless it
+      // ends in the old end state its successor must be revisited
+      a.seg_served[(size_t)k * J + ln.job] = served;
+      a.seg_fsum[(size_t)k * J + ln.job] = fsum;
+      bool same = true;
+      for (int x = 0; x < GS; ++x) same &= bits_of(E_in[own + (size_t)x * J]) == bits_of(s.F[x * 64 + lane]);
+      if (!same) {
+        for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = s.F[x * 64 + lane];
+        atomicAdd(a.changed + q, 1);
+        return;
+      }
     }
   }
   for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = E_in[own + (size_t)x * J];
@@ -700,14 +744,13 @@ __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg,
 }
 
 template <int SMAX, int MB>
-hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, size_t lds2_u, size_t lds2_g,
-                           hipStream_t s) {
+hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.njb * a.nseg)), block(64);
   hipLaunchKernelGGL((spec_pass0<SMAX, MB, true>), grid, block, lds_u, s, a);
   hipLaunchKernelGGL((spec_pass0<SMAX, MB, false>), grid, block, lds_g, s, a);
   for (int q = 1; q < a.nseg; ++q) {
-    hipLaunchKernelGGL((spec_round<SMAX, MB, true>), grid, block, lds2_u, s, a, q);
-    hipLaunchKernelGGL((spec_round<SMAX, MB, false>), grid, block, lds2_g, s, a, q);
+    hipLaunchKernelGGL((spec_round<SMAX, MB, true>), grid, block, lds_u, s, a, q);
+    hipLaunchKernelGGL((spec_round<SMAX, MB, false>), grid, block, lds_g, s, a, q);
   }
   hipLaunchKernelGGL(spec_final, dim3((unsigned)((a.J + 63) / 64)), block, 0, s, a);
   return hipGetLastError();
@@ -725,16 +768,14 @@ int spec_occupancy(size_t lds) {
 
 template <int SMAX>
 int spec_occupancy_mb(int G, size_t lds) {
-  if (G <= 16) return spec_occupancy<SMAX, 16>(lds);
   if (G <= 32) return spec_occupancy<SMAX, 32>(lds);
   return spec_occupancy<SMAX, 64>(lds);
 }
 
 template <int SMAX>
-hipError_t spec_launch_mb(int G, const SpecArgs& a, size_t l1, size_t l2, size_t l3, size_t l4, hipStream_t s) {
-  if (G <= 16) return spec_launch_all<SMAX, 16>(a, l1, l2, l3, l4, s);
-  if (G <= 32) return spec_launch_all<SMAX, 32>(a, l1, l2, l3, l4, s);
-  return spec_launch_all<SMAX, 64>(a, l1, l2, l3, l4, s);
+hipError_t spec_launch_mb(int G, const SpecArgs& a, size_t l1, size_t l2, hipStream_t s) {
+  if (G <= 32) return spec_launch_all<SMAX, 32>(a, l1, l2, s);
+  return spec_launch_all<SMAX, 64>(a, l1, l2, s);
 }
 
 }  // namespace
@@ -772,6 +813,7 @@ void keep_pool_memory() {
 
 constexpr int64_t kSpecMinSegment = 32768;  // requests per segment by default
 constexpr int64_t kSpecWarmup = 32768;      // warm-up requests before a segment
+constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
 
 }  // namespace
 
@@ -791,6 +833,26 @@ int spec_segments(int64_t n, int64_t J, int per_cu) {
   return (int)std::max<int64_t>(1, std::min<int64_t>(k, as_dev::kSpecMaxSeg));
 }
 
+// Whether the speculative kernels beat the shared-trace kernel on this call,
+// by a cost model in cycles per request of one wavefront, measured on gfx950
+// with the 8192-placement, 3.6 M-request workload: the shared-trace kernel
+// about 300 cycles with one wavefront per SIMD and 195 per wavefront beyond
+// that (it is issue-bound there); the speculative kernels about 1150 (one
+// wavefront per SIMD: the LDS holds no more) over a segment plus its warm-up,
+// and a fifth more for the rounds.  A single segment never pays.
+bool spec_pays(const KArgs& k, int nseg, int per_cu) {
+  if (nseg < 2) return false;
+  const double simds = 4.0 * compute_units();
+  const int Wp = pow2ceil(k.G);
+  const double waves_shared = std::ceil((double)k.J / (64 / Wp));
+  const double t_shared = (double)k.n * std::max(300.0, 195.0 * waves_shared / simds);
+  const double slots = (double)compute_units() * std::max(per_cu, 1);
+  const double waves_spec = std::ceil(k.J / 64.0) * nseg;
+  const double seg = (double)k.n / nseg + (double)std::min<int64_t>(kSpecWarmup, k.n);
+  const double t_spec = seg * 1150.0 * 1.2 * std::ceil(waves_spec / slots);
+  return t_spec < t_shared;
+}
+
 // Shared-trace simulation on the segment-speculative kernels.  Returns
 // AS_E_LIMITS without launching when the state of one wavefront (two, in the
 // lockstep rounds) does not fit in the LDS.
@@ -798,11 +860,9 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   using namespace as_dev;
   if (k.n <= 0 || k.J <= 0) return AS_E_LIMITS;
   const size_t lim = shared_lds_limit();
-  const size_t lds_u = spec_lds_bytes(k.M, k.C, k.G, smax, true, 1);
-  const size_t lds_g = spec_lds_bytes(k.M, k.C, k.G, smax, false, 1);
-  const size_t lds2_u = spec_lds_bytes(k.M, k.C, k.G, smax, true, 2);
-  const size_t lds2_g = spec_lds_bytes(k.M, k.C, k.G, smax, false, 2);
-  if (lds2_g > lim) return AS_E_LIMITS;
+  const size_t lds_u = spec_lds_bytes(k.M, k.C, k.G, smax, true);
+  const size_t lds_g = spec_lds_bytes(k.M, k.C, k.G, smax, false);
+  if (lds_g > lim || lds_u > lim) return AS_E_LIMITS;
 
   SpecArgs a;
   std::memset(&a, 0, sizeof a);
@@ -836,8 +896,12 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
     default: per_cu = spec_occupancy_mb<8>(k.G, lds_u); break;
   }
   a.nseg = spec_segments(k.n, k.J, per_cu);
+  if (!spec_forced() && !spec_pays(k, a.nseg, per_cu)) return AS_E_LIMITS;
   a.warmup = kSpecWarmup;
   if (const char* w = getenv("ALPASERVE_SPEC_WARMUP")) a.warmup = std::max<int64_t>(0, atoll(w));
+  a.ck = kSpecCheckpoint;
+  if (const char* c = getenv("ALPASERVE_SPEC_CKPT")) a.ck = std::max<int64_t>(64, atoll(c) & ~(int64_t)63);
+  a.ckps = (int32_t)((k.n / a.nseg + 64) / a.ck + 1);
   while (a.nseg > 1 && (int64_t)a.njb * a.nseg > 0x7FFFFFFFLL) --a.nseg;
   if ((int64_t)a.njb * a.nseg > 0x7FFFFFFFLL) return AS_E_LIMITS;
   a.nw = (k.n + 63) / 64;
@@ -846,9 +910,12 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   const size_t b_bitmap = (size_t)a.nw * J * 8;
   const size_t b_state = (size_t)a.nseg * GS * J * 8;
   const size_t b_seg = (size_t)a.nseg * J * 8;
+  const size_t b_ckpt = (size_t)a.nseg * a.ckps * GS * J * 8;
+  const size_t b_cks = (size_t)a.nseg * a.ckps * J * 8;
   const size_t b_small = 256 + (size_t)a.nseg * 4;
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t total = up(b_bitmap) + up(b_state) + up(2 * b_state) + 2 * up(b_seg) + up(b_small);
+  const size_t total = up(b_bitmap) + up(b_state) + up(2 * b_state) + 2 * up(b_seg) + up(b_ckpt) +
+                       2 * up(b_cks) + up(b_small);
   // a workspace beyond a quarter of the device's memory leaves the call to
   // the kernels that need none
   size_t free_b = 0, total_b = 0;
@@ -869,6 +936,9 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   a.st_end = reinterpret_cast<double*>(take(2 * b_state));
   a.seg_served = reinterpret_cast<int64_t*>(take(b_seg));
   a.seg_fsum = reinterpret_cast<uint64_t*>(take(b_seg));
+  a.ckpt = reinterpret_cast<double*>(take(b_ckpt));
+  a.ck_served = reinterpret_cast<int64_t*>(take(b_cks));
+  a.ck_fsum = reinterpret_cast<uint64_t*>(take(b_cks));
   int32_t* small = reinterpret_cast<int32_t*>(take(b_small));
   a.cfg_info = small;
   a.changed = small + 64;
@@ -876,10 +946,10 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   hipLaunchKernelGGL(spec_cfg_check, dim3(1), dim3(1024), 0, stream, k.group_cfg, (int64_t)k.P * k.G, k.C,
                      a.cfg_info);
   switch (smax) {
-    case 1: e = spec_launch_mb<1>(k.G, a, lds_u, lds_g, lds2_u, lds2_g, stream); break;
-    case 2: e = spec_launch_mb<2>(k.G, a, lds_u, lds_g, lds2_u, lds2_g, stream); break;
-    case 4: e = spec_launch_mb<4>(k.G, a, lds_u, lds_g, lds2_u, lds2_g, stream); break;
-    default: e = spec_launch_mb<8>(k.G, a, lds_u, lds_g, lds2_u, lds2_g, stream); break;
+    case 1: e = spec_launch_mb<1>(k.G, a, lds_u, lds_g, stream); break;
+    case 2: e = spec_launch_mb<2>(k.G, a, lds_u, lds_g, stream); break;
+    case 4: e = spec_launch_mb<4>(k.G, a, lds_u, lds_g, stream); break;
+    default: e = spec_launch_mb<8>(k.G, a, lds_u, lds_g, stream); break;
   }
   const hipError_t ef = hipFreeAsync(ws, stream);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
