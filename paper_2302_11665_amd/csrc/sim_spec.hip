@@ -811,8 +811,10 @@ void keep_pool_memory() {
   done[dev] = true;
 }
 
-constexpr int64_t kSpecMinSegment = 32768;  // requests per segment by default
-constexpr int64_t kSpecWarmup = 32768;      // warm-up requests before a segment
+constexpr int64_t kSpecWarmup = 32768;  // warm-up requests before a segment
+// requests per segment at least: the warm-up and the rounds' re-runs stay a
+// small part of a segment's work
+constexpr int64_t kSpecMinSegment = 4 * kSpecWarmup;
 constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
 
 }  // namespace
