@@ -54,6 +54,11 @@ namespace as_dev {
 namespace {
 
 constexpr int kSpecMaxSeg = 64;
+// Jobs per wavefront: one lane per job.  (32 jobs per wavefront halves the
+// state, so a SIMD holds two wavefronts; on the 8192-placement workload that
+// took 305 ms against 276: the two did not overlap enough to pay for doubling
+// the instructions per job.)
+constexpr int kSpecJobsPerWave = 64;
 constexpr uint64_t kSpecHashMul = 0x9E3779B97F4A7C15ULL;
 
 struct SpecArgs {
@@ -183,13 +188,14 @@ template <int SMAX, bool UCFG>
 struct SpecLds {
   double* T;      // UCFG: [M][SMAX + 1]; else L: [M][C][SMAX]
   double* D;      // !UCFG: [M]
-  uint16_t* cfg;  // !UCFG: [G][64] = c | S << 8
-  double* F;      // [G][SMAX][64]
+  uint16_t* cfg;  // !UCFG: [G][JPW] = c | S << 8
+  double* F;      // [G][SMAX][JPW]
 };
 
-__host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg) {
-  return (ucfg ? (size_t)M * (SMAX + 1) * 8 : (size_t)M * C * SMAX * 8 + (size_t)M * 8 + (size_t)G * 64 * 2) +
-         (size_t)G * SMAX * 64 * 8;
+// jpw: jobs per wavefront (32 or 64); lanes at or above it hold no job
+__host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg, int jpw) {
+  return (ucfg ? (size_t)M * (SMAX + 1) * 8 : (size_t)M * C * SMAX * 8 + (size_t)M * 8 + (size_t)G * jpw * 2) +
+         (size_t)G * SMAX * jpw * 8;
 }
 
 __device__ __forceinline__ double readlane_f64(double v, int l) {
@@ -198,7 +204,7 @@ __device__ __forceinline__ double readlane_f64(double v, int l) {
   return __hiloint2double(hi, lo);
 }
 
-template <int SMAX, bool UCFG>
+template <int SMAX, bool UCFG, int JPW>
 __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, double* lds, int lane, int p,
                                                            bool valid, int c0) {
   SpecLds<SMAX, UCFG> s;
@@ -218,7 +224,7 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
   } else {
     s.D = s.T + (size_t)M * C * SMAX;
     s.cfg = reinterpret_cast<uint16_t*>(s.D + M);
-    s.F = reinterpret_cast<double*>(s.cfg + (size_t)a.G * 64);
+    s.F = reinterpret_cast<double*>(s.cfg + (size_t)a.G * JPW);
     // stage latencies (0 beyond S_c: never used)
     for (int e = lane; e < M * C * SMAX; e += 64) {
       const int k = e % SMAX;
@@ -227,11 +233,12 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
       s.T[e] = k < a.cfg_stages[c] ? a.stage_lat[((int64_t)m * C + c) * a.smax_in + k] : 0.0;
     }
     for (int m = lane; m < M; m += 64) s.D[m] = a.d_single[m];
-    for (int g = 0; g < a.G; ++g) {
-      int c = valid ? a.group_cfg[(int64_t)p * a.G + g] : -1;
-      if (c < 0 || c >= C) c = 0;  // a group hosting nothing is never chosen
-      s.cfg[g * 64 + lane] = (uint16_t)(c | (a.cfg_stages[c] << 8));
-    }
+    if (lane < JPW)
+      for (int g = 0; g < a.G; ++g) {
+        int c = valid ? a.group_cfg[(int64_t)p * a.G + g] : -1;
+        if (c < 0 || c >= C) c = 0;  // a group hosting nothing is never chosen
+        s.cfg[g * JPW + lane] = (uint16_t)(c | (a.cfg_stages[c] << 8));
+      }
   }
   __syncthreads();
   return s;
@@ -278,15 +285,15 @@ struct Reads {
   double d;
 };
 
-template <int SMAX, bool UCFG, int MB>
+template <int SMAX, bool UCFG, int MB, int JPW>
 __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
                                                          int lane) {
   constexpr int kX = Reads<SMAX, UCFG>::kX;
   Reads<SMAX, UCFG> rd;
 #pragma unroll
   for (int k = 0; k < SMAX; ++k) {
-    rd.A[k] = s.F[(pl.g0 * SMAX + k) * 64 + lane];
-    rd.B[k] = s.F[(pl.g1 * SMAX + k) * 64 + lane];
+    rd.A[k] = s.F[(pl.g0 * SMAX + k) * JPW + lane];
+    rd.B[k] = s.F[(pl.g1 * SMAX + k) * JPW + lane];
   }
   rd.extra = __builtin_amdgcn_ballot_w64(pl.more) != 0;
   if (rd.extra) {
@@ -298,7 +305,7 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
       rest &= rest - 1;
     }
 #pragma unroll
-    for (int q = 0; q < kX; ++q) rd.X[q] = s.F[(rd.hx[q] * SMAX) * 64 + lane];
+    for (int q = 0; q < kX; ++q) rd.X[q] = s.F[(rd.hx[q] * SMAX) * JPW + lane];
   }
   const int mi = (unsigned)pl.m < 64u ? pl.m : 0;
   if constexpr (UCFG) {
@@ -316,7 +323,7 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
 // ties), stage chain, admission (finish <= t + scale * d_single[m]) and
 // commit of one request on the lane's state.  Returns the finish time (-1
 // dropped, -2 no hosting group); gs is the group committed to, -1 if none.
-template <int SMAX, bool UCFG, int MB>
+template <int SMAX, bool UCFG, int MB, int JPW>
 __device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
                                               const Reads<SMAX, UCFG>& rd, int lane, double scale, int C, int S0,
                                               int& gs) {
@@ -345,7 +352,7 @@ __device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, cons
       while (rest) {
         const int h = ctz_any(rest);
         rest &= rest - 1;
-        const double v = s.F[(h * SMAX) * 64 + lane];
+        const double v = s.F[(h * SMAX) * JPW + lane];
         if (v < best) {
           best = v;
           g = h;
@@ -354,7 +361,7 @@ __device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, cons
     }
     if (g != pl.g0 && g != pl.g1) {
 #pragma unroll
-      for (int k = 0; k < SMAX; ++k) Fv[k] = s.F[(g * SMAX + k) * 64 + lane];
+      for (int k = 0; k < SMAX; ++k) Fv[k] = s.F[(g * SMAX + k) * JPW + lane];
     }
   }
   double Lv[SMAX];
@@ -363,7 +370,7 @@ __device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, cons
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) Lv[k] = rd.L[k];
   } else {
-    const uint32_t e = s.cfg[g * 64 + lane];
+    const uint32_t e = s.cfg[g * JPW + lane];
     const int c = (int)(e & 0xFF);
     S = (int)(e >> 8);
     const int mi = (unsigned)pl.m < 64u ? pl.m : 0;
@@ -395,7 +402,7 @@ __device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, cons
   if (pl.mask == 0) return -2.0;
   if (prev > deadline) return -1.0;
 #pragma unroll
-  for (int k = 0; k < SMAX; ++k) s.F[(g * SMAX + k) * 64 + lane] = f[k];
+  for (int k = 0; k < SMAX; ++k) s.F[(g * SMAX + k) * JPW + lane] = f[k];
   gs = g;
   return prev;
 }
@@ -406,10 +413,11 @@ struct SpecLane {
   double scale;
 };
 
+template <int JPW>
 __device__ __forceinline__ SpecLane spec_lane(const SpecArgs& a, int jb, int lane) {
   SpecLane l;
-  l.job = jb * 64 + lane;
-  l.valid = l.job < a.J;
+  l.job = jb * JPW + lane;
+  l.valid = lane < JPW && l.job < a.J;
   l.p = l.valid ? l.job / a.K : 0;
   l.scale = l.valid ? a.slo_scale[l.job % a.K] : 0.0;
   l.frow = -1;
@@ -445,12 +453,13 @@ struct TraceChunks {
 // reads.  Per chunk of 64 requests: chunk_begin(base) may stop the loop
 // (returns false once no lane of the wavefront is active), result(i, r, out,
 // gs) sees every simulated request, chunk_end(base, cnt) closes the chunk.
-template <int SMAX, int MB, bool UCFG, class Begin, class Result, class End>
+template <int SMAX, int MB, bool UCFG, int JPW, class Begin, class Result, class End>
 __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
                                            const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int S0,
                                            int64_t from, int64_t to, const bool& active, Begin chunk_begin,
                                            Result result, End chunk_end) {
   if (from >= to) return;
+  const int li = lane & (JPW - 1);  // lanes past JPW hold no job: they read a valid lane's slot
   TraceChunks tc;
   tc.first(a, from, to, lane);
   tc.advance(a, from + 64, lane);
@@ -461,7 +470,7 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
     const bool last_chunk = cb + 64 >= to;
     for (int r = 0; r < cnt; ++r) {
       Reads<SMAX, UCFG> rd;
-      if (active) rd = issue_reads<SMAX, UCFG, MB>(s, cur, lane);
+      if (active) rd = issue_reads<SMAX, UCFG, MB, JPW>(s, cur, li);
       // the next request (the next chunk's first at the end of a chunk; past
       // the range a placeholder), prepared while this one's reads are in
       // flight
@@ -477,7 +486,7 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
       const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, m_nx);
       if (active) {
         int gs;
-        const double out = finish_step<SMAX, UCFG, MB>(s, cur, rd, lane, ln.scale, a.C, S0, gs);
+        const double out = finish_step<SMAX, UCFG, MB, JPW>(s, cur, rd, li, ln.scale, a.C, S0, gs);
         result(cb + r, r, out, gs);
       }
       cur = nxt;
@@ -491,7 +500,7 @@ __device__ __forceinline__ int spec_ckpts(int64_t b, int64_t e, int64_t ck) { re
 
 // Pass 0: every (job, segment) from a warmed-up estimate of its start state;
 // the state is also saved every ck requests (checkpoints for the rounds).
-template <int SMAX, int MB, bool UCFG>
+template <int SMAX, int MB, bool UCFG, int JPW>
 __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   // both variants are launched; the one that does not match the placements
   // returns at once
@@ -501,12 +510,13 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const int lane = threadIdx.x;
   const int jb = blockIdx.x % a.njb;
   const int k = blockIdx.x / a.njb;
-  const SpecLane ln = spec_lane(a, jb, lane);
+  const SpecLane ln = spec_lane<JPW>(a, jb, lane);
   LaneMasks<MB> msk;
   msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-  const auto s = spec_tables<SMAX, UCFG>(a, lds, lane, ln.p, ln.valid, c0);
+  const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int GS = a.G * SMAX;
-  for (int q = 0; q < GS; ++q) s.F[q * 64 + lane] = 0.0;
+  if (lane < JPW)
+    for (int q = 0; q < GS; ++q) s.F[q * JPW + lane] = 0.0;
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   if (blockIdx.x == 0 && lane < a.nseg) a.changed[lane] = lane == 0 ? 1 : 0;
   const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
@@ -525,14 +535,14 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const size_t ck0 = (size_t)k * a.ckps;
   if (w0 == b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
-  spec_range<SMAX, MB, UCFG>(
+  spec_range<SMAX, MB, UCFG, JPW>(
       a, s, msk, ln, lane, S0, w0, e, on,
       [&](int64_t cb) {
         if (cb == b && w0 < b && ln.valid)
-          for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * 64 + lane];
+          for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * JPW + lane];
         if (cb > b && (cb - b) % a.ck == 0 && ln.valid) {
           const size_t j = ck0 + (size_t)((cb - b) / a.ck - 1);
-          for (int q = 0; q < GS; ++q) a.ckpt[(j * GS + q) * J + ln.job] = s.F[q * 64 + lane];
+          for (int q = 0; q < GS; ++q) a.ckpt[(j * GS + q) * J + ln.job] = s.F[q * JPW + lane];
           a.ck_served[j * J + ln.job] = served;
           a.ck_fsum[j * J + ln.job] = fsum;
         }
@@ -553,9 +563,9 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
       });
   // an empty segment's start state is its warm-up end
   if (b == e && w0 < b && ln.valid)
-    for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * 64 + lane];
+    for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * JPW + lane];
   if (!ln.valid) return;
-  for (int q = 0; q < GS; ++q) a.st_end[seg_base + (size_t)q * J] = s.F[q * 64 + lane];  // buffer 0
+  for (int q = 0; q < GS; ++q) a.st_end[seg_base + (size_t)q * J] = s.F[q * JPW + lane];  // buffer 0
   a.seg_served[(size_t)k * J + ln.job] = served;
   a.seg_fsum[(size_t)k * J + ln.job] = fsum;
 }
@@ -566,7 +576,7 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
 // coincide from there on, so the re-run stops and only its prefix replaces
 // the old results.  Checkpoints passed before that point are replaced with
 // the new run's.
-template <int SMAX, int MB, bool UCFG>
+template <int SMAX, int MB, bool UCFG, int JPW>
 __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   if ((a.cfg_info[0] != 0) != UCFG) return;
   if (a.changed[q - 1] == 0) return;  // nothing moved in the previous round: done
@@ -575,7 +585,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   const int lane = threadIdx.x;
   const int jb = blockIdx.x % a.njb;
   const int k = blockIdx.x / a.njb;
-  const SpecLane ln = spec_lane(a, jb, lane);
+  const SpecLane ln = spec_lane<JPW>(a, jb, lane);
   const int GS = a.G * SMAX;
   const int64_t J = a.J;
   const size_t per_buf = (size_t)a.nseg * GS * J;
@@ -596,10 +606,11 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   }
   LaneMasks<MB> msk;
   msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-  const auto s = spec_tables<SMAX, UCFG>(a, lds, lane, ln.p, ln.valid, c0);
+  const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
-  for (int x = 0; x < GS; ++x) s.F[x * 64 + lane] = active ? E_in[prv + (size_t)x * J] : 0.0;
+  if (lane < JPW)
+    for (int x = 0; x < GS; ++x) s.F[x * JPW + lane] = active ? E_in[prv + (size_t)x * J] : 0.0;
 
   const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
   const size_t ck0 = (size_t)k * a.ckps;
@@ -607,7 +618,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
   bool coupled = false;
-  spec_range<SMAX, MB, UCFG>(
+  spec_range<SMAX, MB, UCFG, JPW>(
       a, s, msk, ln, lane, S0, b, e, active,
       [&](int64_t cb) {
         if (cb > b && (cb - b) % a.ck == 0 && active) {
@@ -615,7 +626,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
           const size_t j = ck0 + (size_t)jl;
           bool same = true;
           for (int x = 0; x < GS; ++x)
-            same &= bits_of(a.ckpt[(j * GS + x) * J + ln.job]) == bits_of(s.F[x * 64 + lane]);
+            same &= bits_of(a.ckpt[(j * GS + x) * J + ln.job]) == bits_of(s.F[x * JPW + lane]);
           const int64_t old_s = a.ck_served[j * J + ln.job];
           const uint64_t old_f = a.ck_fsum[j * J + ln.job];
           if (same) {
@@ -634,7 +645,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
               a.ck_fsum[(ck0 + j2) * J + ln.job] += df;
             }
           } else {
-            for (int x = 0; x < GS; ++x) a.ckpt[(j * GS + x) * J + ln.job] = s.F[x * 64 + lane];
+            for (int x = 0; x < GS; ++x) a.ckpt[(j * GS + x) * J + ln.job] = s.F[x * JPW + lane];
             a.ck_served[j * J + ln.job] = served;
             a.ck_fsum[j * J + ln.job] = fsum;
           }
@@ -663,9 +674,9 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
       a.seg_served[(size_t)k * J + ln.job] = served;
       a.seg_fsum[(size_t)k * J + ln.job] = fsum;
       bool same = true;
-      for (int x = 0; x < GS; ++x) same &= bits_of(E_in[own + (size_t)x * J]) == bits_of(s.F[x * 64 + lane]);
+      for (int x = 0; x < GS; ++x) same &= bits_of(E_in[own + (size_t)x * J]) == bits_of(s.F[x * JPW + lane]);
       if (!same) {
-        for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = s.F[x * 64 + lane];
+        for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = s.F[x * JPW + lane];
         atomicAdd(a.changed + q, 1);
         return;
       }
@@ -743,14 +754,14 @@ __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg,
   }
 }
 
-template <int SMAX, int MB>
+template <int SMAX, int MB, int JPW>
 hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.njb * a.nseg)), block(64);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true>), grid, block, lds_u, s, a);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false>), grid, block, lds_g, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW>), grid, block, lds_u, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW>), grid, block, lds_g, s, a);
   for (int q = 1; q < a.nseg; ++q) {
-    hipLaunchKernelGGL((spec_round<SMAX, MB, true>), grid, block, lds_u, s, a, q);
-    hipLaunchKernelGGL((spec_round<SMAX, MB, false>), grid, block, lds_g, s, a, q);
+    hipLaunchKernelGGL((spec_round<SMAX, MB, true, JPW>), grid, block, lds_u, s, a, q);
+    hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW>), grid, block, lds_g, s, a, q);
   }
   hipLaunchKernelGGL(spec_final, dim3((unsigned)((a.J + 63) / 64)), block, 0, s, a);
   return hipGetLastError();
@@ -758,24 +769,23 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
 
 // Workgroups (one wavefront each) of the pass-0 kernel that one compute unit
 // holds at this LDS size.
-template <int SMAX, int MB>
+template <int SMAX, int MB, int JPW>
 int spec_occupancy(size_t lds) {
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true>, 64, lds) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW>, 64, lds) != hipSuccess)
     return 1;
   return nb > 0 ? nb : 1;
 }
 
 template <int SMAX>
 int spec_occupancy_mb(int G, size_t lds) {
-  if (G <= 32) return spec_occupancy<SMAX, 32>(lds);
-  return spec_occupancy<SMAX, 64>(lds);
+  return G <= 32 ? spec_occupancy<SMAX, 32, kSpecJobsPerWave>(lds) : spec_occupancy<SMAX, 64, kSpecJobsPerWave>(lds);
 }
 
 template <int SMAX>
 hipError_t spec_launch_mb(int G, const SpecArgs& a, size_t l1, size_t l2, hipStream_t s) {
-  if (G <= 32) return spec_launch_all<SMAX, 32>(a, l1, l2, s);
-  return spec_launch_all<SMAX, 64>(a, l1, l2, s);
+  return G <= 32 ? spec_launch_all<SMAX, 32, kSpecJobsPerWave>(a, l1, l2, s)
+                 : spec_launch_all<SMAX, 64, kSpecJobsPerWave>(a, l1, l2, s);
 }
 
 }  // namespace
@@ -823,13 +833,13 @@ constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
 // wavefronts to fill the device at the occupancy the LDS allows, each segment
 // long enough that its lockstep prefix is a small part of it.
 // ALPASERVE_SPEC_SEGMENTS forces the count (tests).
-int spec_segments(int64_t n, int64_t J, int per_cu) {
+int spec_segments(int64_t n, int64_t J, int jpw, int per_cu) {
   if (const char* e = getenv("ALPASERVE_SPEC_SEGMENTS")) {
     const int v = atoi(e);
     if (v >= 1) return std::min(v, as_dev::kSpecMaxSeg);
   }
   const int64_t slots = (int64_t)compute_units() * std::max(per_cu, 1);
-  const int64_t njb = (J + 63) / 64;
+  const int64_t njb = (J + jpw - 1) / jpw;
   int64_t k = slots / std::max<int64_t>(njb, 1);
   k = std::min<int64_t>(k, n / kSpecMinSegment);
   return (int)std::max<int64_t>(1, std::min<int64_t>(k, as_dev::kSpecMaxSeg));
@@ -842,14 +852,14 @@ int spec_segments(int64_t n, int64_t J, int per_cu) {
 // that (it is issue-bound there); the speculative kernels about 1150 (one
 // wavefront per SIMD: the LDS holds no more) over a segment plus its warm-up,
 // and a fifth more for the rounds.  A single segment never pays.
-bool spec_pays(const KArgs& k, int nseg, int per_cu) {
+bool spec_pays(const KArgs& k, int nseg, int jpw, int per_cu) {
   if (nseg < 2) return false;
   const double simds = 4.0 * compute_units();
   const int Wp = pow2ceil(k.G);
   const double waves_shared = std::ceil((double)k.J / (64 / Wp));
   const double t_shared = (double)k.n * std::max(300.0, 195.0 * waves_shared / simds);
   const double slots = (double)compute_units() * std::max(per_cu, 1);
-  const double waves_spec = std::ceil(k.J / 64.0) * nseg;
+  const double waves_spec = std::ceil((double)k.J / jpw) * nseg;
   const double seg = (double)k.n / nseg + (double)std::min<int64_t>(kSpecWarmup, k.n);
   const double t_spec = seg * 1150.0 * 1.2 * std::ceil(waves_spec / slots);
   return t_spec < t_shared;
@@ -862,8 +872,9 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   using namespace as_dev;
   if (k.n <= 0 || k.J <= 0) return AS_E_LIMITS;
   const size_t lim = shared_lds_limit();
-  const size_t lds_u = spec_lds_bytes(k.M, k.C, k.G, smax, true);
-  const size_t lds_g = spec_lds_bytes(k.M, k.C, k.G, smax, false);
+  const int jpw = kSpecJobsPerWave;
+  const size_t lds_u = spec_lds_bytes(k.M, k.C, k.G, smax, true, jpw);
+  const size_t lds_g = spec_lds_bytes(k.M, k.C, k.G, smax, false, jpw);
   if (lds_g > lim || lds_u > lim) return AS_E_LIMITS;
 
   SpecArgs a;
@@ -889,7 +900,7 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   a.n_finish = k.n_finish;
   std::memcpy(a.cfg_stages, k.cfg_stages, sizeof a.cfg_stages);
   std::memcpy(a.finish_jobs, k.finish_jobs, sizeof a.finish_jobs);
-  a.njb = (int32_t)((k.J + 63) / 64);
+  a.njb = (int32_t)((k.J + jpw - 1) / jpw);
   int per_cu = 1;
   switch (smax) {
     case 1: per_cu = spec_occupancy_mb<1>(k.G, lds_u); break;
@@ -897,8 +908,8 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
     case 4: per_cu = spec_occupancy_mb<4>(k.G, lds_u); break;
     default: per_cu = spec_occupancy_mb<8>(k.G, lds_u); break;
   }
-  a.nseg = spec_segments(k.n, k.J, per_cu);
-  if (!spec_forced() && !spec_pays(k, a.nseg, per_cu)) return AS_E_LIMITS;
+  a.nseg = spec_segments(k.n, k.J, jpw, per_cu);
+  if (!spec_forced() && !spec_pays(k, a.nseg, jpw, per_cu)) return AS_E_LIMITS;
   a.warmup = kSpecWarmup;
   if (const char* w = getenv("ALPASERVE_SPEC_WARMUP")) a.warmup = std::max<int64_t>(0, atoll(w));
   a.ck = kSpecCheckpoint;
