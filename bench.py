@@ -51,18 +51,18 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "c3abe15bd5f58bce6b7d324ba9004847a79241e86d9894da6e65609b1fcbc682",
+    "sources_sha256": "df62006a1b21c7655a793dd4d2b09be15e27e21035f60de62bcc5fccf64a98b0",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
     "kernel": "spec_pass0<4, 32, true> + spec_round + spec_final + spec_cfg_check",
-    "fetch_kib": 2207452.4375, "write_kib": 5973958.125,
+    "fetch_kib": 2185306.875, "write_kib": 5973958.125,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "c3abe15bd5f58bce6b7d324ba9004847a79241e86d9894da6e65609b1fcbc682",
+    "sources_sha256": "df62006a1b21c7655a793dd4d2b09be15e27e21035f60de62bcc5fccf64a98b0",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595231.6875, "write_kib": 13847.875,
+    "fetch_kib": 2595233.125, "write_kib": 13847.3125,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 

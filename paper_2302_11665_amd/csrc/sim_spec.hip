@@ -696,17 +696,27 @@ __global__ __launch_bounds__(64) void spec_final(const SpecArgs a) {
     served += a.seg_served[(size_t)k * J + job];
     fsum += a.seg_fsum[(size_t)k * J + job];
   }
+  // the hash is sequential over words: the next 16 words are loaded while
+  // the current 16 are folded in
+  constexpr int kB = 16;
   uint64_t h = 0;
   const uint64_t* col = a.bitmap + job;
-  int64_t w = 0;
-  for (; w + 4 <= a.nw; w += 4) {
-    const uint64_t x0 = col[(w + 0) * J], x1 = col[(w + 1) * J], x2 = col[(w + 2) * J], x3 = col[(w + 3) * J];
-    h = (h ^ x0) * kSpecHashMul;
-    h = (h ^ x1) * kSpecHashMul;
-    h = (h ^ x2) * kSpecHashMul;
-    h = (h ^ x3) * kSpecHashMul;
+  const int64_t nb = a.nw / kB;
+  uint64_t cur[kB], nxt[kB];
+  if (nb > 0) {
+#pragma unroll
+    for (int q = 0; q < kB; ++q) cur[q] = col[(int64_t)q * J];
   }
-  for (; w < a.nw; ++w) h = (h ^ col[w * J]) * kSpecHashMul;
+  for (int64_t bi = 0; bi < nb; ++bi) {
+    const int64_t nbase = (bi + 1 < nb ? bi + 1 : bi) * kB;
+#pragma unroll
+    for (int q = 0; q < kB; ++q) nxt[q] = col[(nbase + q) * J];
+#pragma unroll
+    for (int q = 0; q < kB; ++q) h = (h ^ cur[q]) * kSpecHashMul;
+#pragma unroll
+    for (int q = 0; q < kB; ++q) cur[q] = nxt[q];
+  }
+  for (int64_t w = nb * kB; w < a.nw; ++w) h = (h ^ col[w * J]) * kSpecHashMul;
   a.out_served[job] = served;
   if (a.out_attain) a.out_attain[job] = a.n > 0 ? (double)served / (double)a.n : 0.0;
   if (a.out_digest) {
