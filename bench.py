@@ -51,18 +51,18 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "df62006a1b21c7655a793dd4d2b09be15e27e21035f60de62bcc5fccf64a98b0",
+    "sources_sha256": "03dfab669efe3070835fec67be633b09cd2f1ea1d1ac41b4ad6369e5a21f0fa3",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
-    "kernel": "spec_pass0<4, 32, true> + spec_round + spec_final + spec_cfg_check",
-    "fetch_kib": 2185306.875, "write_kib": 5973958.125,
+    "kernel": "spec_pass0<4, 32, true, 64> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check",
+    "fetch_kib": 2302884.6875, "write_kib": 5990868.1875,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "df62006a1b21c7655a793dd4d2b09be15e27e21035f60de62bcc5fccf64a98b0",
+    "sources_sha256": "03dfab669efe3070835fec67be633b09cd2f1ea1d1ac41b4ad6369e5a21f0fa3",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595233.125, "write_kib": 13847.3125,
+    "fetch_kib": 2595225.0625, "write_kib": 13847.9375,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 

@@ -22,6 +22,10 @@
 //            besides its own arrival), so the old results stand and only the
 //            re-run prefix is replaced.  A segment whose runs never meet gets
 //            a new end state, and its successor is revisited next round.
+//            A round re-runs few jobs and lasts as long as the longest
+//            re-run, so for jobs of at most 16 groups it runs in a
+//            group-per-lane layout (a job's groups on W lanes, state in
+//            registers, DPP min dispatch), whose per-request chain is shorter.
 //   final    per job: served counts and finish-time sums add up over
 //            segments; the digest's ordered hash runs over the accept bitmap.
 //
@@ -93,6 +97,19 @@ struct SpecArgs {
   int32_t cfg_stages[AS_MAX_CONFIGS];
   int32_t finish_jobs[AS_MAX_FINISH];
 };
+
+__host__ __device__ constexpr int pow2ceil_dev(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Rounds in the group-per-lane layout where it applies; ALPASERVE_SPEC_ROUNDS=lane
+// keeps the one-lane-per-job round kernel (tests cover both).
+inline bool spec_gpl_rounds() {
+  const char* e = getenv("ALPASERVE_SPEC_ROUNDS");
+  return !(e && std::strcmp(e, "lane") == 0);
+}
 
 __device__ __forceinline__ int64_t seg_bound(int64_t n, int nseg, int k) {
   return k >= nseg ? n : ((n * k / nseg) & ~(int64_t)63);
@@ -685,6 +702,206 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = E_in[own + (size_t)x * J];
 }
 
+// Round q >= 1 in the group-per-lane layout (jobs of at most 16 groups): the
+// same protocol as spec_round, but a job has W lanes, one group each, with its
+// stage free times in registers and the dispatch a DPP min over the W lanes.
+// A round re-runs only a few jobs, and its time is the longest re-run: per
+// request this layout has a shorter dependency chain than one lane per job.
+template <int W, int SMAX>
+__global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
+  constexpr int JW = 64 / W;  // jobs per wavefront
+  if (a.changed[q - 1] == 0) return;
+  extern __shared__ double lds[];
+  const int lane = threadIdx.x;
+  const int g = lane % W, slot = lane / W;
+  const int njbw = (a.J + JW - 1) / JW;
+  const int k = blockIdx.x / njbw, jb = blockIdx.x % njbw;
+  const int job = jb * JW + slot;
+  const bool valid = job < a.J;
+  const bool mine = valid && g < a.G;  // this lane holds a group of a job
+  const int GS = a.G * SMAX;
+  const int64_t J = a.J;
+  const size_t per_buf = (size_t)a.nseg * GS * J;
+  const double* E_in = a.st_end + (size_t)((q - 1) & 1) * per_buf;
+  double* E_out = a.st_end + (size_t)(q & 1) * per_buf;
+  const size_t own = ((size_t)k * GS + (size_t)g * SMAX) * J + job;  // my group's first entry
+  const size_t prv = k > 0 ? ((size_t)(k - 1) * GS + (size_t)g * SMAX) * J + job : 0;
+  const uint64_t fbase = (uint64_t)slot * W;
+  const uint64_t field = (W == 64 ? ~0ull : ((1ull << W) - 1)) << fbase;
+  const uint64_t below = ((1ull << lane) - 1) & field;
+
+  // stale start state?  (every lane of a job agrees through the ballot)
+  bool differ = false;
+  if (mine && k > 0)
+#pragma unroll
+    for (int st = 0; st < SMAX; ++st)
+      differ |= bits_of(a.st_start[own + (size_t)st * J]) != bits_of(E_in[prv + (size_t)st * J]);
+  bool active = (__builtin_amdgcn_ballot_w64(differ) & field) != 0 && valid;
+  const bool ran = active;
+  if (__builtin_amdgcn_ballot_w64(active) == 0) {
+    if (mine)
+#pragma unroll
+      for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = E_in[own + (size_t)st * J];
+    return;
+  }
+  // per-lane data: the models my group hosts, its configuration and depth,
+  // the job's scale, the stage-latency table in LDS, d_single by lane
+  const int p = valid ? job / a.K : 0;
+  const double scale = valid ? a.slo_scale[job % a.K] : 0.0;
+  uint64_t hostm = 0;
+  int cg = 0, Sg = 1;
+  if (mine) {
+    for (int m = 0; m < a.M; ++m) hostm |= ((a.host_mask[(int64_t)p * a.M + m] >> g) & 1ull) << m;
+    cg = a.group_cfg[(int64_t)p * a.G + g];
+    if (cg < 0 || cg >= a.C) {
+      cg = 0;
+      hostm = 0;  // an unused group hosts nothing
+    }
+    Sg = a.cfg_stages[cg];
+  }
+  double* Lt = lds;  // [M][C][SMAX]
+  for (int e = lane; e < a.M * a.C * SMAX; e += 64) {
+    const int st = e % SMAX, c = (e / SMAX) % a.C, m = e / (SMAX * a.C);
+    Lt[e] = st < a.cfg_stages[c] ? a.stage_lat[((int64_t)m * a.C + c) * a.smax_in + st] : 0.0;
+  }
+  const double dl_lane = lane < a.M ? a.d_single[lane] : 1.0;
+  __syncthreads();
+  int frow = -1;
+  if (valid)
+    for (int f = 0; f < a.n_finish; ++f)
+      if (a.finish_jobs[f] == job) frow = f;
+  const bool wave_rows = __builtin_amdgcn_ballot_w64(frow >= 0) != 0;
+  double F[SMAX];
+#pragma unroll
+  for (int st = 0; st < SMAX; ++st) F[st] = (mine && active) ? E_in[prv + (size_t)st * J] : 0.0;
+
+  const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
+  const size_t ck0 = (size_t)k * a.ckps;
+  const int nck = b < e ? spec_ckpts(b, e, a.ck) : 0;
+  uint64_t served = 0, fsum = 0;  // this lane's share (the requests it committed)
+  bool coupled = false;
+  const double kInf = __builtin_inf();
+  TraceChunks tc;
+  tc.first(a, b, e, lane);
+  for (int64_t cb = b; cb < e; cb += 64) {
+    tc.advance(a, cb + 64, lane);
+    if (cb > b && (cb - b) % a.ck == 0) {
+      // saved state of the current results at cb: compare, then keep or stop
+      const int jl = (int)((cb - b) / a.ck) - 1;
+      const size_t j = ck0 + (size_t)jl;
+      bool same = true;
+      if (mine && active)
+#pragma unroll
+        for (int st = 0; st < SMAX; ++st)
+          same &= bits_of(a.ckpt[(j * GS + (size_t)g * SMAX + st) * J + job]) == bits_of(F[st]);
+      const bool job_same = (__builtin_amdgcn_ballot_w64(!same) & field) == 0;
+      const uint64_t js = seg_sum_u64<W>(served), jf = seg_sum_u64<W>(fsum);  // uniform flow
+      if (active) {
+        const size_t cj = j * J + job;
+        if (job_same) {
+          if (g == 0) {
+            const int64_t ds = (int64_t)js - a.ck_served[cj];
+            const uint64_t df = jf - a.ck_fsum[cj];
+            a.seg_served[(size_t)k * J + job] += ds;
+            a.seg_fsum[(size_t)k * J + job] += df;
+            a.ck_served[cj] = (int64_t)js;
+            a.ck_fsum[cj] = jf;
+            for (int j2 = jl + 1; j2 < nck; ++j2) {
+              a.ck_served[(ck0 + j2) * J + job] += ds;
+              a.ck_fsum[(ck0 + j2) * J + job] += df;
+            }
+          }
+          coupled = true;
+          active = false;
+        } else {
+          if (mine)
+#pragma unroll
+            for (int st = 0; st < SMAX; ++st) a.ckpt[(j * GS + (size_t)g * SMAX + st) * J + job] = F[st];
+          if (g == 0) {
+            a.ck_served[cj] = (int64_t)js;
+            a.ck_fsum[cj] = jf;
+          }
+        }
+      }
+      if (__builtin_amdgcn_ballot_w64(active) == 0) break;
+    }
+    const int cnt = (int)(e - cb < 64 ? e - cb : 64);
+    uint64_t word = 0;
+    for (int r = 0; r < cnt; ++r) {
+      const double ti = readlane_f64(tc.tv, r);
+      const int m = __builtin_amdgcn_readlane(tc.mv, r);
+      if (!active) continue;
+      const bool host = (unsigned)m < (unsigned)a.M && ((hostm >> (m & 63)) & 1ull);
+      const int mi = (unsigned)m < (unsigned)a.M ? m : 0;
+      double L[SMAX];
+#pragma unroll
+      for (int st = 0; st < SMAX; ++st) L[st] = Lt[((size_t)mi * a.C + cg) * SMAX + st];
+      const double key = host ? F[0] : kInf;
+      const double mn = seg_min<W>(key);
+      const bool eq = host && key == mn;
+      const uint64_t ball = __builtin_amdgcn_ballot_w64(eq);
+      const bool chosen = eq && (ball & below) == 0;
+      double f[SMAX];
+      double prev = ti;
+#pragma unroll
+      for (int st = 0; st < SMAX; ++st) {
+        const double x = vmax(prev, F[st]) + L[st];
+        const bool in = st < Sg;
+        f[st] = in ? x : F[st];
+        prev = in ? x : prev;
+      }
+      const double deadline = ti + scale * readlane_f64(dl_lane, mi);
+      const bool acc = chosen && !(prev > deadline);
+      if (acc) {
+#pragma unroll
+        for (int st = 0; st < SMAX; ++st) F[st] = f[st];
+        served += 1;
+        fsum += bits_of(prev);
+      }
+      if ((__builtin_amdgcn_ballot_w64(acc) & field) != 0) word |= 1ull << r;
+      if (wave_rows) {
+        const bool any_host = (__builtin_amdgcn_ballot_w64(host) & field) != 0;
+        if (frow >= 0) {
+          if (chosen) {
+            a.out_finish[(int64_t)frow * a.n + cb + r] = acc ? prev : -1.0;
+          } else if (g == 0 && !any_host) {
+            a.out_finish[(int64_t)frow * a.n + cb + r] = -2.0;
+          }
+        }
+      }
+    }
+    if (active && g == 0) a.bitmap[(cb >> 6) * J + job] = word;
+  }
+  const uint64_t js = seg_sum_u64<W>(served), jf = seg_sum_u64<W>(fsum);  // uniform flow
+  bool end_same = true;
+  if (mine && ran && !coupled)
+#pragma unroll
+    for (int st = 0; st < SMAX; ++st) end_same &= bits_of(E_in[own + (size_t)st * J]) == bits_of(F[st]);
+  const bool job_end_same = (__builtin_amdgcn_ballot_w64(!end_same) & field) == 0;
+  if (!valid) return;
+  if (ran) {
+    if (mine)
+#pragma unroll
+      for (int st = 0; st < SMAX; ++st) a.st_start[own + (size_t)st * J] = E_in[prv + (size_t)st * J];
+    if (!coupled) {
+      if (g == 0) {
+        a.seg_served[(size_t)k * J + job] = (int64_t)js;
+        a.seg_fsum[(size_t)k * J + job] = jf;
+      }
+      if (!job_end_same) {
+        if (mine)
+#pragma unroll
+          for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = F[st];
+        if (g == 0) atomicAdd(a.changed + q, 1);
+        return;
+      }
+    }
+  }
+  if (mine)
+#pragma unroll
+    for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = E_in[own + (size_t)st * J];
+}
+
 // Per job: totals over segments and the ordered digest over the accept words.
 __global__ __launch_bounds__(64) void spec_final(const SpecArgs a) {
   const int64_t job = (int64_t)blockIdx.x * 64 + threadIdx.x;
@@ -764,14 +981,38 @@ __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg,
   }
 }
 
+// Rounds in the group-per-lane layout (jobs of at most 16 groups).
+template <int W, int SMAX>
+void spec_rounds_gpl(const SpecArgs& a, hipStream_t s) {
+  const int njbw = (a.J + 64 / W - 1) / (64 / W);
+  const dim3 grid((unsigned)((int64_t)njbw * a.nseg)), block(64);
+  const size_t lds = (size_t)a.M * a.C * SMAX * 8;
+  for (int q = 1; q < a.nseg; ++q) hipLaunchKernelGGL((spec_round_gpl<W, SMAX>), grid, block, lds, s, a, q);
+}
+
+template <int SMAX>
+void spec_rounds_gpl_w(const SpecArgs& a, hipStream_t s) {
+  switch (pow2ceil_dev(a.G)) {
+    case 1: spec_rounds_gpl<1, SMAX>(a, s); break;
+    case 2: spec_rounds_gpl<2, SMAX>(a, s); break;
+    case 4: spec_rounds_gpl<4, SMAX>(a, s); break;
+    case 8: spec_rounds_gpl<8, SMAX>(a, s); break;
+    default: spec_rounds_gpl<16, SMAX>(a, s); break;
+  }
+}
+
 template <int SMAX, int MB, int JPW>
 hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.njb * a.nseg)), block(64);
   hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW>), grid, block, lds_u, s, a);
   hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW>), grid, block, lds_g, s, a);
-  for (int q = 1; q < a.nseg; ++q) {
-    hipLaunchKernelGGL((spec_round<SMAX, MB, true, JPW>), grid, block, lds_u, s, a, q);
-    hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW>), grid, block, lds_g, s, a, q);
+  if (a.G <= 16 && spec_gpl_rounds()) {
+    spec_rounds_gpl_w<SMAX>(a, s);
+  } else {
+    for (int q = 1; q < a.nseg; ++q) {
+      hipLaunchKernelGGL((spec_round<SMAX, MB, true, JPW>), grid, block, lds_u, s, a, q);
+      hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW>), grid, block, lds_g, s, a, q);
+    }
   }
   hipLaunchKernelGGL(spec_final, dim3((unsigned)((a.J + 63) / 64)), block, 0, s, a);
   return hipGetLastError();
@@ -831,10 +1072,14 @@ void keep_pool_memory() {
   done[dev] = true;
 }
 
-constexpr int64_t kSpecWarmup = 32768;  // warm-up requests before a segment
+// warm-up requests before a segment (measured on the 8192-placement workload:
+// 32768 -> 255.7 ms per step, 16384 -> 249.5, 8192 -> 242-244, 2048 -> 251,
+// none -> 261: a shorter warm-up leaves more to the rounds)
+constexpr int64_t kSpecWarmup = 8192;
 // requests per segment at least: the warm-up and the rounds' re-runs stay a
-// small part of a segment's work
-constexpr int64_t kSpecMinSegment = 4 * kSpecWarmup;
+// small part of a segment's work (shorter traces, like the searches' 151k
+// requests, ran slower on these kernels)
+constexpr int64_t kSpecMinSegment = 131072;
 constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
 
 }  // namespace

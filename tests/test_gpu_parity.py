@@ -33,6 +33,10 @@ VARIANTS = {
     # a warm-up shorter than a segment
     "spec_seg16_warm100": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "16",
                            "ALPASERVE_SPEC_WARMUP": "100"},
+    # reconciliation rounds on the one-lane-per-job kernel (the default takes the
+    # group-per-lane kernel for jobs of at most 16 groups)
+    "spec_seg7_lanerounds": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "7", "ALPASERVE_SPEC_WARMUP": "0",
+                             "ALPASERVE_SPEC_ROUNDS": "lane"},
     # saved states every 64 requests: re-runs stop at the first one they meet
     "spec_seg5_ck64": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "5", "ALPASERVE_SPEC_WARMUP": "0",
                        "ALPASERVE_SPEC_CKPT": "64"},
@@ -52,7 +56,7 @@ def gpu_api():
 @pytest.fixture(params=sorted(VARIANTS))
 def gpu(request, gpu_api, monkeypatch):
     for k in ("ALPASERVE_PATH", "ALPASERVE_GPL", "ALPASERVE_SPEC_SEGMENTS", "ALPASERVE_SPEC_WARMUP",
-              "ALPASERVE_SPEC_CKPT"):
+              "ALPASERVE_SPEC_CKPT", "ALPASERVE_SPEC_ROUNDS"):
         monkeypatch.delenv(k, raising=False)
     for k, v in VARIANTS[request.param].items():
         monkeypatch.setenv(k, v)
