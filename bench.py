@@ -51,7 +51,7 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "03dfab669efe3070835fec67be633b09cd2f1ea1d1ac41b4ad6369e5a21f0fa3",
+    "sources_sha256": "96c902d8b417d0e00337bcc8059c1100fe41d374fa98903fc76e514e2ff1532c",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
@@ -60,7 +60,7 @@ MEASURED_TRAFFIC = {
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "03dfab669efe3070835fec67be633b09cd2f1ea1d1ac41b4ad6369e5a21f0fa3",
+    "sources_sha256": "96c902d8b417d0e00337bcc8059c1100fe41d374fa98903fc76e514e2ff1532c",
     "kernel": "seg_kernel<1>",
     "fetch_kib": 2595225.0625, "write_kib": 13847.9375,
     "fetch_scale": 1048576.0 / 524299.5, "write_scale": 1048576.0 / 1048576.0,

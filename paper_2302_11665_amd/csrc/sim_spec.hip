@@ -209,7 +209,7 @@ struct SpecLds {
   double* F;      // [G][SMAX][JPW]
 };
 
-// jpw: jobs per wavefront (32 or 64); lanes at or above it hold no job
+// jpw: jobs per wavefront (lanes at or above it hold no job)
 __host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg, int jpw) {
   return (ucfg ? (size_t)M * (SMAX + 1) * 8 : (size_t)M * C * SMAX * 8 + (size_t)M * 8 + (size_t)G * jpw * 2) +
          (size_t)G * SMAX * jpw * 8;
@@ -1086,7 +1086,7 @@ constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
 
 // Segments per job for the speculative path: enough (job block, segment)
 // wavefronts to fill the device at the occupancy the LDS allows, each segment
-// long enough that its lockstep prefix is a small part of it.
+// long enough that the warm-up and the rounds' re-runs are a small part of it.
 // ALPASERVE_SPEC_SEGMENTS forces the count (tests).
 int spec_segments(int64_t n, int64_t J, int jpw, int per_cu) {
   if (const char* e = getenv("ALPASERVE_SPEC_SEGMENTS")) {
@@ -1121,8 +1121,10 @@ bool spec_pays(const KArgs& k, int nseg, int jpw, int per_cu) {
 }
 
 // Shared-trace simulation on the segment-speculative kernels.  Returns
-// AS_E_LIMITS without launching when the state of one wavefront (two, in the
-// lockstep rounds) does not fit in the LDS.
+// AS_E_LIMITS without launching when the state of one wavefront does not fit
+// in the LDS, when the trace does not split into segments that pay (unless
+// ALPASERVE_PATH=spec forces the kernels), or when the workspace would be too
+// large.
 int run_spec(KArgs& k, int smax, hipStream_t stream) {
   using namespace as_dev;
   if (k.n <= 0 || k.J <= 0) return AS_E_LIMITS;
