@@ -206,13 +206,15 @@ struct SpecLds {
   double* T;      // UCFG: [M][SMAX + 1]; else L: [M][C][SMAX]
   double* D;      // !UCFG: [M]
   uint16_t* cfg;  // !UCFG: [G][JPW] = c | S << 8
-  double* F;      // [G][SMAX][JPW]
+  double* F;      // [G + 1][SMAX][JPW]; row G is written, never read
 };
 
-// jpw: jobs per wavefront (lanes at or above it hold no job)
+// jpw: jobs per wavefront (lanes at or above it hold no job).  The state has
+// one spare row past the G groups: a request that commits nothing writes
+// there, so that the commit is a store without a branch.
 __host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg, int jpw) {
   return (ucfg ? (size_t)M * (SMAX + 1) * 8 : (size_t)M * C * SMAX * 8 + (size_t)M * 8 + (size_t)G * jpw * 2) +
-         (size_t)G * SMAX * jpw * 8;
+         (size_t)(G + 1) * SMAX * jpw * 8;
 }
 
 __device__ __forceinline__ double readlane_f64(double v, int l) {
@@ -263,8 +265,8 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
 
 // The wavefront-uniform part of a request and this lane's hosting groups:
 // arrival t, model m, hosting mask, the two lowest hosting groups (both the
-// lowest when there is one; 0 when there is none) and whether the lane has
-// more.
+// lowest when there is one; 0 when there is none) and whether any lane of the
+// wavefront has more.
 template <int MB>
 struct Plan {
   using MaskT = typename LaneMasks<MB>::MaskT;
@@ -272,7 +274,7 @@ struct Plan {
   int m;
   MaskT mask;
   int g0, g1;
-  bool more;
+  bool extra;  // some lane of the wavefront has more than two hosting groups
 };
 
 template <int MB>
@@ -281,11 +283,12 @@ __device__ __forceinline__ Plan<MB> make_plan(const SpecArgs& a, const LaneMasks
   pl.t = t;
   pl.m = m;
   const bool known = (unsigned)m < (unsigned)a.M;
-  pl.mask = known ? msk.get(m) : 0;
+  const auto x = msk.get(m);  // register moves only: cheaper than a branch around them
+  pl.mask = known ? x : 0;
   const auto r1 = pl.mask & (pl.mask - 1);
   pl.g0 = pl.mask ? ctz_any(pl.mask) : 0;
   pl.g1 = r1 ? ctz_any(r1) : pl.g0;
-  pl.more = (r1 & (r1 - 1)) != 0;
+  pl.extra = __builtin_amdgcn_ballot_w64((r1 & (r1 - 1)) != 0) != 0;
   return pl;
 }
 
@@ -312,7 +315,7 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
     rd.A[k] = s.F[(pl.g0 * SMAX + k) * JPW + lane];
     rd.B[k] = s.F[(pl.g1 * SMAX + k) * JPW + lane];
   }
-  rd.extra = __builtin_amdgcn_ballot_w64(pl.more) != 0;
+  rd.extra = pl.extra;
   if (rd.extra) {
     auto rest = pl.mask & (pl.mask - 1);
     rest &= rest - 1;
@@ -338,12 +341,13 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
 
 // Dispatch (least stage-0 free time among the hosting groups, lowest index on
 // ties), stage chain, admission (finish <= t + scale * d_single[m]) and
-// commit of one request on the lane's state.  Returns the finish time (-1
-// dropped, -2 no hosting group); gs is the group committed to, -1 if none.
+// commit of one request on the lane's state.  Returns whether the request is
+// served (never on an inactive lane); out is its finish time (-1 dropped, -2
+// no hosting group).  Requests that are not served write the spare row G.
 template <int SMAX, bool UCFG, int MB, int JPW>
-__device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
-                                              const Reads<SMAX, UCFG>& rd, int lane, double scale, int C, int S0,
-                                              int& gs) {
+__device__ __forceinline__ bool finish_step(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
+                                            const Reads<SMAX, UCFG>& rd, int lane, double scale, int C, int G,
+                                            int S0, bool active, double& out) {
   constexpr int kX = Reads<SMAX, UCFG>::kX;
   // g1 > g0, and further hosts come in increasing order: strict comparisons
   // keep the lowest index among equal free times
@@ -415,13 +419,13 @@ __device__ __forceinline__ double finish_step(const SpecLds<SMAX, UCFG>& s, cons
   }
   const double slo = scale * rd.d;
   const double deadline = pl.t + slo;
-  gs = -1;
-  if (pl.mask == 0) return -2.0;
-  if (prev > deadline) return -1.0;
+  const bool hosted = pl.mask != 0;
+  const bool served = active && hosted && !(prev > deadline);
+  out = served ? prev : (hosted ? -1.0 : -2.0);
+  const int row = served ? g : G;
 #pragma unroll
-  for (int k = 0; k < SMAX; ++k) s.F[(g * SMAX + k) * JPW + lane] = f[k];
-  gs = g;
-  return prev;
+  for (int k = 0; k < SMAX; ++k) s.F[(row * SMAX + k) * JPW + lane] = f[k];
+  return served;
 }
 
 struct SpecLane {
@@ -469,7 +473,8 @@ struct TraceChunks {
 // with the next request's preparation overlapping the current one's LDS
 // reads.  Per chunk of 64 requests: chunk_begin(base) may stop the loop
 // (returns false once no lane of the wavefront is active), result(i, r, out,
-// gs) sees every simulated request, chunk_end(base, cnt) closes the chunk.
+// served) sees every simulated request (on an inactive lane with served
+// false and out meaningless), chunk_end(base, cnt) closes the chunk.
 template <int SMAX, int MB, bool UCFG, int JPW, class Begin, class Result, class End>
 __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
                                            const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int S0,
@@ -485,27 +490,29 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
     if (!chunk_begin(cb)) return;
     const int cnt = (int)(to - cb < 64 ? to - cb : 64);
     const bool last_chunk = cb + 64 >= to;
+    // lane r: the request after request r (lane 63: the next chunk's first;
+    // past the range a placeholder)
+    const int from_lane = ((lane + 1) & 63) << 2;
+    int t1_lo = __builtin_amdgcn_ds_bpermute(from_lane, __double2loint(tc.tv));
+    int t1_hi = __builtin_amdgcn_ds_bpermute(from_lane, __double2hiint(tc.tv));
+    int m1 = __builtin_amdgcn_ds_bpermute(from_lane, tc.mv);
+    const int n_lo = __builtin_amdgcn_readlane(__double2loint(tc.tn), 0);
+    const int n_hi = __builtin_amdgcn_readlane(__double2hiint(tc.tn), 0);
+    const int n_m = __builtin_amdgcn_readlane(tc.mn, 0);
+    if (lane == 63) {
+      t1_lo = n_lo;
+      t1_hi = n_hi;
+      m1 = n_m;
+    }
     for (int r = 0; r < cnt; ++r) {
-      Reads<SMAX, UCFG> rd;
-      if (active) rd = issue_reads<SMAX, UCFG, MB, JPW>(s, cur, li);
-      // the next request (the next chunk's first at the end of a chunk; past
-      // the range a placeholder), prepared while this one's reads are in
-      // flight
-      double t_nx;
-      int m_nx;
-      if (r + 1 < cnt) {
-        t_nx = readlane_f64(tc.tv, r + 1);
-        m_nx = __builtin_amdgcn_readlane(tc.mv, r + 1);
-      } else {
-        t_nx = readlane_f64(tc.tn, 0);
-        m_nx = __builtin_amdgcn_readlane(tc.mn, 0);
-      }
-      const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, m_nx);
-      if (active) {
-        int gs;
-        const double out = finish_step<SMAX, UCFG, MB, JPW>(s, cur, rd, li, ln.scale, a.C, S0, gs);
-        result(cb + r, r, out, gs);
-      }
+      const Reads<SMAX, UCFG> rd = issue_reads<SMAX, UCFG, MB, JPW>(s, cur, li);
+      // the next request, prepared while this one's reads are in flight
+      const double t_nx =
+          __hiloint2double(__builtin_amdgcn_readlane(t1_hi, r), __builtin_amdgcn_readlane(t1_lo, r));
+      const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
+      double out;
+      const bool served = finish_step<SMAX, UCFG, MB, JPW>(s, cur, rd, li, ln.scale, a.C, a.G, S0, active, out);
+      result(cb + r, r, out, served);
       cur = nxt;
     }
     chunk_end(cb, cnt);
@@ -549,12 +556,19 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const size_t seg_base = ((size_t)k * GS) * J + ln.job;
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
+  bool rows_now = false;  // this chunk lies in the segment and the wavefront has finish rows
   const size_t ck0 = (size_t)k * a.ckps;
   if (w0 == b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
   spec_range<SMAX, MB, UCFG, JPW>(
       a, s, msk, ln, lane, S0, w0, e, on,
       [&](int64_t cb) {
+        if (cb == b) {
+          // the warm-up counts nothing
+          served = 0;
+          fsum = 0;
+        }
+        rows_now = wave_rows && cb >= b;
         if (cb == b && w0 < b && ln.valid)
           for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * JPW + lane];
         if (cb > b && (cb - b) % a.ck == 0 && ln.valid) {
@@ -565,22 +579,23 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
         }
         return true;
       },
-      [&](int64_t i, int r, double out, int gs) {
-        if (i < b) return;
-        if (gs >= 0) {
-          served += 1;
-          fsum += bits_of(out);
-          word |= 1ull << r;
-        }
-        if (wave_rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+      [&](int64_t i, int r, double out, bool sv) {
+        fsum += sv ? bits_of(out) : 0;
+        word |= (uint64_t)sv << r;
+        if (rows_now && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [&](int64_t cb, int) {
         if (cb >= b && ln.valid) a.bitmap[(cb >> 6) * J + ln.job] = word;
+        served += __popcll(word);
         word = 0;
       });
-  // an empty segment's start state is its warm-up end
+  // an empty segment's start state is its warm-up end, and it counts nothing
   if (b == e && w0 < b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * JPW + lane];
+  if (b == e) {
+    served = 0;
+    fsum = 0;
+  }
   if (!ln.valid) return;
   for (int q = 0; q < GS; ++q) a.st_end[seg_base + (size_t)q * J] = s.F[q * JPW + lane];  // buffer 0
   a.seg_served[(size_t)k * J + ln.job] = served;
@@ -669,16 +684,14 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
         }
         return __builtin_amdgcn_ballot_w64(active) != 0;
       },
-      [&](int64_t i, int r, double out, int gs) {
-        if (gs >= 0) {
-          served += 1;
-          fsum += bits_of(out);
-          word |= 1ull << r;
-        }
-        if (wave_rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+      [&](int64_t i, int r, double out, bool sv) {
+        fsum += sv ? bits_of(out) : 0;
+        word |= (uint64_t)sv << r;
+        if (wave_rows && ln.frow >= 0 && active) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [&](int64_t cb, int) {
         if (active) a.bitmap[(cb >> 6) * J + ln.job] = word;
+        served += __popcll(word);
         word = 0;
       });
   if (!ln.valid) return;
