@@ -303,8 +303,10 @@ __global__ void validate_kernel(const double* t, const int32_t* model, int64_t n
   if (bad) atomicOr(flags, bad);
 }
 
-// Fill p[0, n) with v (per-request output rows before a shared-trace launch).
-__global__ void fill_f64(double* __restrict__ p, int64_t n, double v) {
+// Fill p[0, n) with v (per-request output rows before a shared-trace launch);
+// nothing when gate is set and *gate == 0.
+__global__ void fill_f64(double* __restrict__ p, int64_t n, double v, const int32_t* gate) {
+  if (gate && *gate == 0) return;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     p[i] = v;
@@ -338,19 +340,15 @@ int run_shared_stats(KArgs& a, int smax, hipStream_t stream) {
   return ok();
 }
 
-// Launch the batched simulation of a shared trace (a fully filled except the
-// kernel shape).  W is the group count on entry.
-int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
+// The shared-trace kernel (one group per lane, W = G rounded up to a power of
+// two) unless its tables exceed the LDS of a workgroup; then the general
+// kernel, whose tables are smaller.  With only_check, whether one of them
+// takes the call (AS_OK) or not (AS_E_LIMITS), without launching.
+int run_trace_kernels(KArgs& a, int W, int smax, hipStream_t stream, bool only_check) {
   const int64_t J = a.J;
-  if (want_spec(a, smax)) {
-    const int rc = run_spec(a, smax, stream);
-    if (rc != AS_E_LIMITS) return rc;
-  }
-  // shared-trace kernel (one group per lane, W = G rounded up to a power of
-  // two) unless its tables exceed the LDS of a workgroup; then the general
-  // kernel, whose tables are smaller
   const size_t lds_shared = as_dev::shared_lds_bytes(a.M, pow2ceil(a.C), smax);
   if (use_shared_path() && lds_shared <= shared_lds_limit()) {
+    if (only_check) return AS_OK;
     const int Ws = pow2ceil(a.G);
     hipError_t e = hipSuccess;
     if (a.n_finish > 0 && a.n > 0) {
@@ -358,7 +356,7 @@ int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
       const int64_t cells = (int64_t)a.n_finish * a.n;
       const int64_t blocks = std::min<int64_t>((cells + 255) / 256, 8192);
       hipLaunchKernelGGL(fill_f64, dim3((unsigned)blocks), dim3(256), 0, stream, a.out_finish,
-                         cells, -2.0);
+                         cells, -2.0, a.gate);
       if ((e = hipGetLastError()) != hipSuccess)
         return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     }
@@ -368,12 +366,40 @@ int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
   }
   int GPL = 1;
   if (!choose_shape(a.G, J, false, a.M, a.C, smax, W, GPL))
-    return fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
-                a.M, a.C, smax);
+    return only_check ? AS_E_LIMITS
+                      : fail(AS_E_LIMITS, "stage-latency tables (%d models x %d configs x %d stages) do not fit in LDS",
+                             a.M, a.C, smax);
+  if (only_check) return AS_OK;
   const size_t lds = lds_bytes(W, smax, false, a.M, a.C);
   hipError_t e = launch_lds_any(W, GPL, smax, false, a, lds, stream);
   if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+// Launch the batched simulation of a shared trace (a fully filled except the
+// kernel shape).  W is the group count on entry.  The segment-speculative
+// kernels go first where they take the call; when one of their re-runs gives
+// up (traffic under which runs from different states do not meet), the
+// kernels above, launched behind them and gated on that flag, produce the
+// results instead.  All of it stays stream-ordered: no host synchronisation.
+int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
+  if (want_spec(a, smax)) {
+    const bool fallback = run_trace_kernels(a, W, smax, stream, true) == AS_OK;
+    void* ws = nullptr;
+    const int32_t* gave_up = nullptr;
+    const int rc = run_spec(a, smax, stream, fallback, &ws, &gave_up);
+    if (rc != AS_E_LIMITS) {
+      if (rc != AS_OK || !fallback) return rc;
+      a.gate = gave_up;
+      const int rc2 = run_trace_kernels(a, W, smax, stream, false);
+      a.gate = nullptr;
+      const hipError_t ef = hipFreeAsync(ws, stream);
+      if (rc2 != AS_OK) return rc2;
+      if (ef != hipSuccess) return fail(AS_E_HIP, "workspace release failed: %s", hipGetErrorString(ef));
+      return ok();
+    }
+  }
+  return run_trace_kernels(a, W, smax, stream, false);
 }
 
 }  // namespace as_host

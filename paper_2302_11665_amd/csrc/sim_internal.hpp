@@ -33,8 +33,15 @@ int run_shared_stats(KArgs& a, int smax, hipStream_t stream);
 
 // Shared-trace simulation on the segment-speculative kernels (one lane per
 // job, the trace cut into segments simulated at once and reconciled);
-// AS_E_LIMITS without launching when a wavefront's state does not fit in LDS.
-int run_spec(KArgs& a, int smax, hipStream_t stream);
+// AS_E_LIMITS without launching when a wavefront's state does not fit in LDS
+// or the segments would not pay.  With can_give_up, a reconciliation re-run
+// that has not met the old results after a bounded number of requests stops
+// the pipeline and sets *gave_up (device memory) to 1, else it stays 0: the
+// caller then launches other kernels gated on it, which produce all results,
+// and releases *workspace (stream-ordered, hipFreeAsync) after them.  Without
+// it the workspace is released here and *gave_up is null.
+int run_spec(KArgs& a, int smax, hipStream_t stream, bool can_give_up, void** workspace,
+             const int32_t** gave_up);
 // Whether a shared-trace call takes the segment-speculative kernels.
 bool want_spec(const KArgs& a, int smax);
 // Whether ALPASERVE_PATH=spec forces them (even with a single segment).

@@ -76,6 +76,9 @@ struct KArgs {
   int32_t P, n_segments;
   int32_t cfg_stages[AS_MAX_CONFIGS];
   int32_t finish_jobs[AS_MAX_FINISH];
+  // set: the launch does nothing unless *gate != 0 (the speculative kernels'
+  // give-up flag, when these kernels stand behind them)
+  const int32_t* gate;
 };
 
 __device__ __forceinline__ double vmax(double a, double b) {
@@ -279,6 +282,7 @@ __device__ __forceinline__ void run_chunk(LaneState<GPL, SMAX>& st, const LaneCo
 
 template <int W, int GPL, int SMAX, bool SEG>
 __global__ __launch_bounds__(kThreads) void sim_kernel(const KArgs a) {
+  if (a.gate && *a.gate == 0) return;
   constexpr int JW = 64 / W;           // jobs per wavefront
   constexpr int kSlots = JW * kWaves;  // jobs per workgroup
   constexpr int CH = SEG ? seg_chunk<kSlots>() : kChunk;

@@ -308,6 +308,7 @@ __host__ __device__ constexpr size_t shared_stats_lds_bytes(int W, int M) {
 // JW = 64/W.  Per-request output rows must hold -2 when the kernel starts.
 template <int W, int SMAX, bool USIG, bool STATS = false>
 __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
+  if (a.gate && *a.gate == 0) return;
   constexpr int JW = 64 / W;
   constexpr int kSlots = JW * kWaves;
   constexpr int RSH = rec_shift(SMAX);

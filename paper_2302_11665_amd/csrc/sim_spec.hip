@@ -58,6 +58,15 @@ namespace as_dev {
 namespace {
 
 constexpr int kSpecMaxSeg = 64;
+// A reconciliation re-run that has not met the old results after this many
+// requests gives up, and the call falls back to the shared-trace kernels.  On
+// bursty traffic runs from different states meet within a few thousand
+// requests (on the 8192-placement heavy trace a cap of 32,768 gives up and one
+// of 65,536 does not); where groups stay saturated they may never meet, and
+// every round would then re-run whole segments (that heavy trace with each
+// model kept on two groups: 2.29 s per call without the cap, 0.92 s with it,
+// 0.56 s on the shared-trace kernel alone).
+constexpr int64_t kSpecGiveUp = 131072;
 // Jobs per wavefront: one lane per job.  (32 jobs per wavefront halves the
 // state, so a SIMD holds two wavefronts; on the 8192-placement workload that
 // took 305 ms against 276: the two did not overlap enough to pay for doubling
@@ -90,7 +99,9 @@ struct SpecArgs {
   int64_t ck;           // checkpoint interval (a multiple of 64)
   int32_t ckps;         // checkpoints per segment (upper bound)
   int32_t* changed;     // [nseg] segments whose end state changed, per round
-  int32_t* cfg_info;    // [2]: 1 when every used group has one configuration; that configuration
+  int32_t* cfg_info;    // [3]: 1 when every used group has one configuration; that configuration;
+                        // 1 once a re-run gave up (the results are then left to other kernels)
+  int64_t cap;          // requests a re-run may take without meeting the old results before giving up
   int64_t nw;
   int64_t warmup;  // requests simulated before a segment to estimate its start state
   int32_t M, C, smax_in, G, K, J, n_finish, nseg, njb;
@@ -117,6 +128,15 @@ __device__ __forceinline__ int64_t seg_bound(int64_t n, int nseg, int k) {
 
 __device__ __forceinline__ uint64_t bits_of(double x) { return (uint64_t)__double_as_longlong(x); }
 
+// Accept bits of a chunk: each request's bit enters at the top and moves down
+// one place per request, so that after the chunk's cnt requests chunk_word
+// has request r's bit at r.
+__device__ __forceinline__ uint64_t push_bit(uint64_t w, bool bit) {
+  const uint32_t lo = (uint32_t)w, hi = (uint32_t)(w >> 32);
+  return ((uint64_t)__builtin_amdgcn_alignbit((uint32_t)bit, hi, 1) << 32) | __builtin_amdgcn_alignbit(hi, lo, 1);
+}
+__device__ __forceinline__ uint64_t chunk_word(uint64_t w, int cnt) { return cnt < 64 ? w >> (64 - cnt) : w; }
+
 // Hosting masks of one lane's placement for every model, MB bits per model,
 // held in vector registers (32-dword vector values: a wavefront-uniform index
 // into one lowers to indexed register moves, not memory).
@@ -142,15 +162,18 @@ struct LaneMasks {
       }
     }
   }
-  // bits of groups >= G are dropped (they name no state)
-  __device__ __forceinline__ void load(const uint64_t* row, int M, int G, bool valid) {
+  // bits of groups >= G are dropped (they name no state); returns whether some
+  // model has more than two hosting groups
+  __device__ __forceinline__ bool load(const uint64_t* row, int M, int G, bool valid) {
     v0 = v1 = (u32x32)(0u);
     if constexpr (MB == 64) v2 = v3 = (u32x32)(0u);
-    if (!valid) return;
+    bool many = false;
+    if (!valid) return many;
     const uint64_t keep = G >= 64 ? ~0ull : (1ull << G) - 1;
 #pragma unroll
     for (int m = 0; m < 64; ++m) {
       const uint64_t x = m < M ? row[m] & keep : 0;
+      many |= __popcll(x) > 2;
       if constexpr (MB == 32) {
         put(m, (uint32_t)x);
       } else {
@@ -158,6 +181,7 @@ struct LaneMasks {
         put(2 * m + 1, (uint32_t)(x >> 32));
       }
     }
+    return many;
   }
   // m is wavefront-uniform; one indexed register move per vector read (the
   // empty asm keeps the compiler from selecting whole vectors first)
@@ -277,7 +301,7 @@ struct Plan {
   bool extra;  // some lane of the wavefront has more than two hosting groups
 };
 
-template <int MB>
+template <int MB, bool EXTRA>
 __device__ __forceinline__ Plan<MB> make_plan(const SpecArgs& a, const LaneMasks<MB>& msk, double t, int m) {
   Plan<MB> pl;
   pl.t = t;
@@ -288,7 +312,7 @@ __device__ __forceinline__ Plan<MB> make_plan(const SpecArgs& a, const LaneMasks
   const auto r1 = pl.mask & (pl.mask - 1);
   pl.g0 = pl.mask ? ctz_any(pl.mask) : 0;
   pl.g1 = r1 ? ctz_any(r1) : pl.g0;
-  pl.extra = __builtin_amdgcn_ballot_w64((r1 & (r1 - 1)) != 0) != 0;
+  pl.extra = EXTRA && __builtin_amdgcn_ballot_w64((r1 & (r1 - 1)) != 0) != 0;
   return pl;
 }
 
@@ -471,11 +495,12 @@ struct TraceChunks {
 
 // Simulate requests [from, to) of one lane (only while the lane is active)
 // with the next request's preparation overlapping the current one's LDS
-// reads.  Per chunk of 64 requests: chunk_begin(base) may stop the loop
+// reads.  EXTRA false: no lane hosts a model on more than two groups.  Per
+// chunk of 64 requests: chunk_begin(base) may stop the loop
 // (returns false once no lane of the wavefront is active), result(i, r, out,
 // served) sees every simulated request (on an inactive lane with served
 // false and out meaningless), chunk_end(base, cnt) closes the chunk.
-template <int SMAX, int MB, bool UCFG, int JPW, class Begin, class Result, class End>
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, class Begin, class Result, class End>
 __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
                                            const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int S0,
                                            int64_t from, int64_t to, const bool& active, Begin chunk_begin,
@@ -485,7 +510,7 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
   TraceChunks tc;
   tc.first(a, from, to, lane);
   tc.advance(a, from + 64, lane);
-  Plan<MB> cur = make_plan<MB>(a, msk, readlane_f64(tc.tv, 0), __builtin_amdgcn_readlane(tc.mv, 0));
+  Plan<MB> cur = make_plan<MB, EXTRA>(a, msk, readlane_f64(tc.tv, 0), __builtin_amdgcn_readlane(tc.mv, 0));
   for (int64_t cb = from; cb < to; cb += 64) {
     if (!chunk_begin(cb)) return;
     const int cnt = (int)(to - cb < 64 ? to - cb : 64);
@@ -509,7 +534,7 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
       // the next request, prepared while this one's reads are in flight
       const double t_nx =
           __hiloint2double(__builtin_amdgcn_readlane(t1_hi, r), __builtin_amdgcn_readlane(t1_lo, r));
-      const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
+      const Plan<MB> nxt = make_plan<MB, EXTRA>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
       double out;
       const bool served = finish_step<SMAX, UCFG, MB, JPW>(s, cur, rd, li, ln.scale, a.C, a.G, S0, active, out);
       result(cb + r, r, out, served);
@@ -524,10 +549,13 @@ __device__ __forceinline__ int spec_ckpts(int64_t b, int64_t e, int64_t ck) { re
 
 // Pass 0: every (job, segment) from a warmed-up estimate of its start state;
 // the state is also saved every ck requests (checkpoints for the rounds).
-template <int SMAX, int MB, bool UCFG, int JPW>
+// Every kernel of the speculative pipeline that simulates requests comes in
+// four variants, all launched: UCFG (all groups of all placements share one
+// configuration) and EXTRA (some lane of the wavefront hosts a model on more
+// than two groups) select the code; a workgroup whose data do not match its
+// variant returns at once, before any side effect.
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA>
 __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
-  // both variants are launched; the one that does not match the placements
-  // returns at once
   if ((a.cfg_info[0] != 0) != UCFG) return;
   const int c0 = UCFG ? a.cfg_info[1] : 0;
   extern __shared__ double lds[];
@@ -536,7 +564,8 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const int k = blockIdx.x / a.njb;
   const SpecLane ln = spec_lane<JPW>(a, jb, lane);
   LaneMasks<MB> msk;
-  msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+  const bool many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+  if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int GS = a.G * SMAX;
   if (lane < JPW)
@@ -560,7 +589,7 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const size_t ck0 = (size_t)k * a.ckps;
   if (w0 == b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
-  spec_range<SMAX, MB, UCFG, JPW>(
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA>(
       a, s, msk, ln, lane, S0, w0, e, on,
       [&](int64_t cb) {
         if (cb == b) {
@@ -581,14 +610,16 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
       },
       [&](int64_t i, int r, double out, bool sv) {
         fsum += sv ? bits_of(out) : 0;
-        word |= (uint64_t)sv << r;
+        word = push_bit(word, sv);
         if (rows_now && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
-      [&](int64_t cb, int) {
+      [&](int64_t cb, int cnt) {
+        word = chunk_word(word, cnt);
         if (cb >= b && ln.valid) a.bitmap[(cb >> 6) * J + ln.job] = word;
         served += __popcll(word);
         word = 0;
       });
+
   // an empty segment's start state is its warm-up end, and it counts nothing
   if (b == e && w0 < b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * JPW + lane];
@@ -608,9 +639,10 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
 // coincide from there on, so the re-run stops and only its prefix replaces
 // the old results.  Checkpoints passed before that point are replaced with
 // the new run's.
-template <int SMAX, int MB, bool UCFG, int JPW>
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA>
 __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   if ((a.cfg_info[0] != 0) != UCFG) return;
+  if (a.cfg_info[2] != 0) return;     // a re-run gave up: other kernels take over
   if (a.changed[q - 1] == 0) return;  // nothing moved in the previous round: done
   const int c0 = UCFG ? a.cfg_info[1] : 0;
   extern __shared__ double lds[];
@@ -625,6 +657,9 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   double* E_out = a.st_end + (size_t)(q & 1) * per_buf;
   const size_t own = ((size_t)k * GS) * J + ln.job;
   const size_t prv = k > 0 ? ((size_t)(k - 1) * GS) * J + ln.job : 0;
+  LaneMasks<MB> msk;
+  const bool many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+  if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
 
   bool active = false;
   if (ln.valid && k > 0)
@@ -636,8 +671,6 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
       for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = E_in[own + (size_t)x * J];
     return;
   }
-  LaneMasks<MB> msk;
-  msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
@@ -649,8 +682,8 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   const int nck = b < e ? spec_ckpts(b, e, a.ck) : 0;
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
-  bool coupled = false;
-  spec_range<SMAX, MB, UCFG, JPW>(
+  bool coupled = false, gave_up = false;
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA>(
       a, s, msk, ln, lane, S0, b, e, active,
       [&](int64_t cb) {
         if (cb > b && (cb - b) % a.ck == 0 && active) {
@@ -682,19 +715,28 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
             a.ck_fsum[j * J + ln.job] = fsum;
           }
         }
-        return __builtin_amdgcn_ballot_w64(active) != 0;
+        const bool any = __builtin_amdgcn_ballot_w64(active) != 0;
+        if (any && cb - b >= a.cap) {
+          // runs from the two states do not meet: the pipeline gives up
+          if (lane == 0) a.cfg_info[2] = 1;
+          gave_up = true;
+          return false;
+        }
+        return any;
       },
       [&](int64_t i, int r, double out, bool sv) {
         fsum += sv ? bits_of(out) : 0;
-        word |= (uint64_t)sv << r;
+        word = push_bit(word, sv);
         if (wave_rows && ln.frow >= 0 && active) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
-      [&](int64_t cb, int) {
+      [&](int64_t cb, int cnt) {
+        word = chunk_word(word, cnt);
         if (active) a.bitmap[(cb >> 6) * J + ln.job] = word;
         served += __popcll(word);
         word = 0;
       });
-  if (!ln.valid) return;
+
+  if (gave_up || !ln.valid) return;
   if (ran) {
     // the predecessor's end state now stands behind this segment's results
     for (int x = 0; x < GS; ++x) a.st_start[own + (size_t)x * J] = E_in[prv + (size_t)x * J];
@@ -723,6 +765,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
 template <int W, int SMAX>
 __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
   constexpr int JW = 64 / W;  // jobs per wavefront
+  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels take over
   if (a.changed[q - 1] == 0) return;
   extern __shared__ double lds[];
   const int lane = threadIdx.x;
@@ -838,6 +881,11 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
       }
       if (__builtin_amdgcn_ballot_w64(active) == 0) break;
     }
+    if (cb - b >= a.cap && __builtin_amdgcn_ballot_w64(active) != 0) {
+      // runs from the two states do not meet: the pipeline gives up
+      if (lane == 0) a.cfg_info[2] = 1;
+      return;
+    }
     const int cnt = (int)(e - cb < 64 ? e - cb : 64);
     uint64_t word = 0;
     for (int r = 0; r < cnt; ++r) {
@@ -917,6 +965,7 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
 
 // Per job: totals over segments and the ordered digest over the accept words.
 __global__ __launch_bounds__(64) void spec_final(const SpecArgs a) {
+  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels write the results
   const int64_t job = (int64_t)blockIdx.x * 64 + threadIdx.x;
   if (job >= a.J) return;
   const int64_t J = a.J;
@@ -962,8 +1011,8 @@ namespace as_dev {
 namespace {
 
 // Whether every group that a placement uses (configuration >= 0) has one and
-// the same configuration; cfg_info = {uniform, that configuration}.  One
-// workgroup of 1024 threads.
+// the same configuration; cfg_info = {uniform, that configuration, 0 (no
+// re-run has given up)}.  One workgroup of 1024 threads.
 __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg, int64_t cells, int n_configs,
                                                        int32_t* cfg_info) {
   __shared__ int lo[1024], hi[1024];
@@ -991,6 +1040,7 @@ __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg,
     // per-lane tables, which clamp them
     cfg_info[0] = none || (lo[0] == hi[0] && lo[0] < n_configs) ? 1 : 0;
     cfg_info[1] = none ? 0 : lo[0];
+    cfg_info[2] = 0;
   }
 }
 
@@ -1017,14 +1067,18 @@ void spec_rounds_gpl_w(const SpecArgs& a, hipStream_t s) {
 template <int SMAX, int MB, int JPW>
 hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.njb * a.nseg)), block(64);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW>), grid, block, lds_u, s, a);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW>), grid, block, lds_g, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false>), grid, block, lds_u, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true>), grid, block, lds_u, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, false>), grid, block, lds_g, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, true>), grid, block, lds_g, s, a);
   if (a.G <= 16 && spec_gpl_rounds()) {
     spec_rounds_gpl_w<SMAX>(a, s);
   } else {
     for (int q = 1; q < a.nseg; ++q) {
-      hipLaunchKernelGGL((spec_round<SMAX, MB, true, JPW>), grid, block, lds_u, s, a, q);
-      hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW>), grid, block, lds_g, s, a, q);
+      hipLaunchKernelGGL((spec_round<SMAX, MB, true, JPW, false>), grid, block, lds_u, s, a, q);
+      hipLaunchKernelGGL((spec_round<SMAX, MB, true, JPW, true>), grid, block, lds_u, s, a, q);
+      hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW, false>), grid, block, lds_g, s, a, q);
+      hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW, true>), grid, block, lds_g, s, a, q);
     }
   }
   hipLaunchKernelGGL(spec_final, dim3((unsigned)((a.J + 63) / 64)), block, 0, s, a);
@@ -1036,7 +1090,7 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
 template <int SMAX, int MB, int JPW>
 int spec_occupancy(size_t lds) {
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW>, 64, lds) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW, false>, 64, lds) != hipSuccess)
     return 1;
   return nb > 0 ? nb : 1;
 }
@@ -1137,9 +1191,13 @@ bool spec_pays(const KArgs& k, int nseg, int jpw, int per_cu) {
 // AS_E_LIMITS without launching when the state of one wavefront does not fit
 // in the LDS, when the trace does not split into segments that pay (unless
 // ALPASERVE_PATH=spec forces the kernels), or when the workspace would be too
-// large.
-int run_spec(KArgs& k, int smax, hipStream_t stream) {
+// large.  With can_give_up the workspace outlives the call: the caller's
+// gated fallback kernels read the give-up flag in it, then release it.
+int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void** workspace,
+             const int32_t** gave_up) {
   using namespace as_dev;
+  *workspace = nullptr;
+  *gave_up = nullptr;
   if (k.n <= 0 || k.J <= 0) return AS_E_LIMITS;
   const size_t lim = shared_lds_limit();
   const int jpw = kSpecJobsPerWave;
@@ -1185,6 +1243,8 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
   a.ck = kSpecCheckpoint;
   if (const char* c = getenv("ALPASERVE_SPEC_CKPT")) a.ck = std::max<int64_t>(64, atoll(c) & ~(int64_t)63);
   a.ckps = (int32_t)((k.n / a.nseg + 64) / a.ck + 1);
+  a.cap = can_give_up ? kSpecGiveUp : INT64_MAX;
+  if (const char* c = getenv("ALPASERVE_SPEC_CAP"); c && can_give_up) a.cap = std::max<int64_t>(64, atoll(c));
   while (a.nseg > 1 && (int64_t)a.njb * a.nseg > 0x7FFFFFFFLL) --a.nseg;
   if ((int64_t)a.njb * a.nseg > 0x7FFFFFFFLL) return AS_E_LIMITS;
   a.nw = (k.n + 63) / 64;
@@ -1234,9 +1294,14 @@ int run_spec(KArgs& k, int smax, hipStream_t stream) {
     case 4: e = spec_launch_mb<4>(k.G, a, lds_u, lds_g, stream); break;
     default: e = spec_launch_mb<8>(k.G, a, lds_u, lds_g, stream); break;
   }
-  const hipError_t ef = hipFreeAsync(ws, stream);
-  if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
-  if (ef != hipSuccess) return fail(AS_E_HIP, "workspace release failed: %s", hipGetErrorString(ef));
+  if (e != hipSuccess || !can_give_up) {
+    const hipError_t ef = hipFreeAsync(ws, stream);
+    if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    if (ef != hipSuccess) return fail(AS_E_HIP, "workspace release failed: %s", hipGetErrorString(ef));
+    return ok();
+  }
+  *workspace = ws;
+  *gave_up = a.cfg_info + 2;
   return ok();
 }
 

@@ -40,6 +40,14 @@ VARIANTS = {
     # saved states every 64 requests: re-runs stop at the first one they meet
     "spec_seg5_ck64": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "5", "ALPASERVE_SPEC_WARMUP": "0",
                        "ALPASERVE_SPEC_CKPT": "64"},
+    # re-runs give up after 64 requests without meeting the old results (cold
+    # segments rarely meet that soon): the shared-trace kernels launched behind
+    # the pipeline, gated on that flag, produce the results; with either
+    # round kernel
+    "spec_seg7_giveup": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "7", "ALPASERVE_SPEC_WARMUP": "0",
+                         "ALPASERVE_SPEC_CAP": "64"},
+    "spec_seg7_giveup_lane": {"ALPASERVE_PATH": "spec", "ALPASERVE_SPEC_SEGMENTS": "7",
+                              "ALPASERVE_SPEC_WARMUP": "0", "ALPASERVE_SPEC_CAP": "64", "ALPASERVE_SPEC_ROUNDS": "lane"},
 }
 
 
@@ -56,7 +64,7 @@ def gpu_api():
 @pytest.fixture(params=sorted(VARIANTS))
 def gpu(request, gpu_api, monkeypatch):
     for k in ("ALPASERVE_PATH", "ALPASERVE_GPL", "ALPASERVE_SPEC_SEGMENTS", "ALPASERVE_SPEC_WARMUP",
-              "ALPASERVE_SPEC_CKPT", "ALPASERVE_SPEC_ROUNDS"):
+              "ALPASERVE_SPEC_CKPT", "ALPASERVE_SPEC_ROUNDS", "ALPASERVE_SPEC_CAP"):
         monkeypatch.delenv(k, raising=False)
     for k, v in VARIANTS[request.param].items():
         monkeypatch.setenv(k, v)
