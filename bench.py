@@ -51,19 +51,19 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "88f7781e9393c3d5b6cfc9ca6c3b0a404668bd6faf11e77154892637c9adce3b",
+    "sources_sha256": "e1ed0330e506a2f23b85389533f900eb7c8f5c7e56ee3e40a5aee5f8ace8a460",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
-    "kernel": "spec_pass0<4, 32, true, 64, true> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check "
+    "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check "
               "(+ the pass-0 variants that return at once)",
-    "fetch_kib": 2157140.4375, "write_kib": 5990871.9375,
+    "fetch_kib": 2159256.0, "write_kib": 5990874.8125,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "88f7781e9393c3d5b6cfc9ca6c3b0a404668bd6faf11e77154892637c9adce3b",
+    "sources_sha256": "e1ed0330e506a2f23b85389533f900eb7c8f5c7e56ee3e40a5aee5f8ace8a460",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595224.625, "write_kib": 13847.96875,
+    "fetch_kib": 2595228.75, "write_kib": 13848.96875,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 

@@ -221,6 +221,19 @@ __device__ __forceinline__ int ctz_any(T x) {
   }
 }
 
+// Index of the lowest set bit, -1 when there is none (v_ffbl_b32 returns
+// all ones for zero; the asm keeps the compiler from assuming x != 0).
+template <typename T>
+__device__ __forceinline__ int lowest_or_m1(T x) {
+  if constexpr (sizeof(T) == 4) {
+    int r;
+    asm("v_ffbl_b32 %0, %1" : "=v"(r) : "v"(x));
+    return r;
+  } else {
+    return x ? (int)__builtin_ctzll(x) : -1;
+  }
+}
+
 // Per-wavefront LDS: the model table, per-lane group configurations when
 // groups differ, then the state.
 //   uniform configuration c0:  T[m] = {L[m][c0][0..SMAX-1], d_single[m]}
@@ -230,15 +243,18 @@ struct SpecLds {
   double* T;      // UCFG: [M][SMAX + 1]; else L: [M][C][SMAX]
   double* D;      // !UCFG: [M]
   uint16_t* cfg;  // !UCFG: [G][JPW] = c | S << 8
-  double* F;      // [G + 1][SMAX][JPW]; row G is written, never read
+  double* F;      // rows -1 .. G of [SMAX][JPW]; row -1 is a sentinel, row G is written, never read
 };
 
 // jpw: jobs per wavefront (lanes at or above it hold no job).  The state has
-// one spare row past the G groups: a request that commits nothing writes
-// there, so that the commit is a store without a branch.
+// a spare row past the G groups: a request that commits nothing writes
+// there, so that the commit is a store without a branch.  Before the groups
+// sits a sentinel row -1 whose stage-0 free time is +inf: a lane that has no
+// (or no further) hosting group reads it as its host, and it never wins the
+// dispatch.
 __host__ __device__ constexpr size_t spec_lds_bytes(int M, int C, int G, int SMAX, bool ucfg, int jpw) {
   return (ucfg ? (size_t)M * (SMAX + 1) * 8 : (size_t)M * C * SMAX * 8 + (size_t)M * 8 + (size_t)G * jpw * 2) +
-         (size_t)(G + 1) * SMAX * jpw * 8;
+         (size_t)(G + 2) * SMAX * jpw * 8;
 }
 
 __device__ __forceinline__ double readlane_f64(double v, int l) {
@@ -256,7 +272,7 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
   if constexpr (UCFG) {
     s.D = nullptr;
     s.cfg = nullptr;
-    s.F = s.T + (size_t)M * (SMAX + 1);
+    s.F = s.T + (size_t)M * (SMAX + 1) + SMAX * JPW;
     const int S0 = a.cfg_stages[c0];
     for (int e = lane; e < M * (SMAX + 1); e += 64) {
       const int k = e % (SMAX + 1);
@@ -267,7 +283,7 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
   } else {
     s.D = s.T + (size_t)M * C * SMAX;
     s.cfg = reinterpret_cast<uint16_t*>(s.D + M);
-    s.F = reinterpret_cast<double*>(s.cfg + (size_t)a.G * JPW);
+    s.F = reinterpret_cast<double*>(s.cfg + (size_t)a.G * JPW) + SMAX * JPW;
     // stage latencies (0 beyond S_c: never used)
     for (int e = lane; e < M * C * SMAX; e += 64) {
       const int k = e % SMAX;
@@ -283,14 +299,15 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
         s.cfg[g * JPW + lane] = (uint16_t)(c | (a.cfg_stages[c] << 8));
       }
   }
+  // the sentinel row: stage 0 never wins, the other stages are never committed
+  for (int e = lane; e < SMAX * JPW; e += 64) s.F[e - SMAX * JPW] = e < JPW ? __builtin_inf() : 0.0;
   __syncthreads();
   return s;
 }
 
 // The wavefront-uniform part of a request and this lane's hosting groups:
-// arrival t, model m, hosting mask, the two lowest hosting groups (both the
-// lowest when there is one; 0 when there is none) and whether any lane of the
-// wavefront has more.
+// arrival t, model m, hosting mask and the two lowest hosting groups (-1, the
+// sentinel row, where there is none).
 template <int MB>
 struct Plan {
   using MaskT = typename LaneMasks<MB>::MaskT;
@@ -298,10 +315,15 @@ struct Plan {
   int m;
   MaskT mask;
   int g0, g1;
-  bool extra;  // some lane of the wavefront has more than two hosting groups
+  // whether some lane of the wavefront hosts the model on more than two
+  // groups (a ballot: wavefront-uniform)
+  __device__ __forceinline__ bool extra() const {
+    const MaskT r1 = mask & (mask - 1);
+    return __builtin_amdgcn_ballot_w64((r1 & (r1 - 1)) != 0) != 0;
+  }
 };
 
-template <int MB, bool EXTRA>
+template <int MB>
 __device__ __forceinline__ Plan<MB> make_plan(const SpecArgs& a, const LaneMasks<MB>& msk, double t, int m) {
   Plan<MB> pl;
   pl.t = t;
@@ -310,15 +332,15 @@ __device__ __forceinline__ Plan<MB> make_plan(const SpecArgs& a, const LaneMasks
   const auto x = msk.get(m);  // register moves only: cheaper than a branch around them
   pl.mask = known ? x : 0;
   const auto r1 = pl.mask & (pl.mask - 1);
-  pl.g0 = pl.mask ? ctz_any(pl.mask) : 0;
-  pl.g1 = r1 ? ctz_any(r1) : pl.g0;
-  pl.extra = EXTRA && __builtin_amdgcn_ballot_w64((r1 & (r1 - 1)) != 0) != 0;
+  pl.g0 = lowest_or_m1(pl.mask);
+  pl.g1 = lowest_or_m1(r1);
   return pl;
 }
 
 // LDS reads of one request, issued together: the rows of the two lowest
 // hosting groups, the stage-0 entries of up to six more hosts when some lane
-// of the wavefront has them, and the model's table row.
+// of the wavefront has them, and the model's table row.  X: 0 never reads the
+// extra hosts, 1 always, 2 when ex (wavefront-uniform) is set.
 template <int SMAX, bool UCFG>
 struct Reads {
   static constexpr int kX = 6;
@@ -329,9 +351,9 @@ struct Reads {
   double d;
 };
 
-template <int SMAX, bool UCFG, int MB, int JPW>
+template <int SMAX, bool UCFG, int MB, int JPW, int X>
 __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
-                                                         int lane) {
+                                                         int lane, bool ex) {
   constexpr int kX = Reads<SMAX, UCFG>::kX;
   Reads<SMAX, UCFG> rd;
 #pragma unroll
@@ -339,13 +361,13 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
     rd.A[k] = s.F[(pl.g0 * SMAX + k) * JPW + lane];
     rd.B[k] = s.F[(pl.g1 * SMAX + k) * JPW + lane];
   }
-  rd.extra = pl.extra;
+  rd.extra = X == 1 || (X == 2 && ex);
   if (rd.extra) {
     auto rest = pl.mask & (pl.mask - 1);
     rest &= rest - 1;
 #pragma unroll
     for (int q = 0; q < kX; ++q) {
-      rd.hx[q] = rest ? ctz_any(rest) : pl.g0;
+      rd.hx[q] = lowest_or_m1(rest);
       rest &= rest - 1;
     }
 #pragma unroll
@@ -368,19 +390,23 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
 // commit of one request on the lane's state.  Returns whether the request is
 // served (never on an inactive lane); out is its finish time (-1 dropped, -2
 // no hosting group).  Requests that are not served write the spare row G.
-template <int SMAX, bool UCFG, int MB, int JPW>
+// X as for issue_reads (rd.extra: the extra hosts were read).  FULL: every
+// group has SMAX stages (a uniform configuration of the deepest kind).
+template <int SMAX, bool UCFG, int MB, int JPW, int X, bool FULL>
 __device__ __forceinline__ bool finish_step(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
                                             const Reads<SMAX, UCFG>& rd, int lane, double scale, int C, int G,
                                             int S0, bool active, double& out) {
+  static_assert(!FULL || UCFG, "FULL needs a uniform configuration");
   constexpr int kX = Reads<SMAX, UCFG>::kX;
   // g1 > g0, and further hosts come in increasing order: strict comparisons
-  // keep the lowest index among equal free times
+  // keep the lowest index among equal free times (a missing host is the
+  // sentinel row, +inf: with no host at all, g is -1 and nothing commits)
   const bool use_b = rd.B[0] < rd.A[0];
   int g = use_b ? pl.g1 : pl.g0;
   double Fv[SMAX];
 #pragma unroll
   for (int k = 0; k < SMAX; ++k) Fv[k] = use_b ? rd.B[k] : rd.A[k];
-  if (rd.extra) {
+  if (X == 1 || (X == 2 && rd.extra)) {
     double best = Fv[0];
 #pragma unroll
     for (int q = 0; q < kX; ++q) {
@@ -415,7 +441,7 @@ __device__ __forceinline__ bool finish_step(const SpecLds<SMAX, UCFG>& s, const 
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) Lv[k] = rd.L[k];
   } else {
-    const uint32_t e = s.cfg[g * JPW + lane];
+    const uint32_t e = s.cfg[(g < 0 ? 0 : g) * JPW + lane];
     const int c = (int)(e & 0xFF);
     S = (int)(e >> 8);
     const int mi = (unsigned)pl.m < 64u ? pl.m : 0;
@@ -426,7 +452,7 @@ __device__ __forceinline__ bool finish_step(const SpecLds<SMAX, UCFG>& s, const 
   // projection through the stage chain; stages past S keep their state
   double f[SMAX];
   double prev = pl.t;
-  if (UCFG && S == SMAX) {
+  if (FULL || (UCFG && S == SMAX)) {
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) {
       f[k] = vmax(prev, Fv[k]) + Lv[k];
@@ -495,12 +521,15 @@ struct TraceChunks {
 
 // Simulate requests [from, to) of one lane (only while the lane is active)
 // with the next request's preparation overlapping the current one's LDS
-// reads.  EXTRA false: no lane hosts a model on more than two groups.  Per
-// chunk of 64 requests: chunk_begin(base) may stop the loop
-// (returns false once no lane of the wavefront is active), result(i, r, out,
-// served) sees every simulated request (on an inactive lane with served
-// false and out meaningless), chunk_end(base, cnt) closes the chunk.
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, class Begin, class Result, class End>
+// reads.  EXTRA false: no lane hosts a model on more than two groups.  ROWS
+// false: no lane writes finish rows (the code for them is left out).  Per
+// chunk of 64 requests: chunk_begin(base) returns 0 to stop the loop (once no
+// lane of the wavefront is active), 1 to run the chunk, 2 to run it with
+// finish rows; result(i, r, out, served, rows) sees every simulated request
+// (on an inactive lane with served false and out meaningless; rows: the chunk
+// writes finish rows), chunk_end(base, cnt) closes the chunk.
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL, bool ROWS, class Begin, class Result,
+          class End>
 __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
                                            const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int S0,
                                            int64_t from, int64_t to, const bool& active, Begin chunk_begin,
@@ -510,9 +539,10 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
   TraceChunks tc;
   tc.first(a, from, to, lane);
   tc.advance(a, from + 64, lane);
-  Plan<MB> cur = make_plan<MB, EXTRA>(a, msk, readlane_f64(tc.tv, 0), __builtin_amdgcn_readlane(tc.mv, 0));
+  Plan<MB> cur = make_plan<MB>(a, msk, readlane_f64(tc.tv, 0), __builtin_amdgcn_readlane(tc.mv, 0));
   for (int64_t cb = from; cb < to; cb += 64) {
-    if (!chunk_begin(cb)) return;
+    const int code = chunk_begin(cb);
+    if (code == 0) return;
     const int cnt = (int)(to - cb < 64 ? to - cb : 64);
     const bool last_chunk = cb + 64 >= to;
     // lane r: the request after request r (lane 63: the next chunk's first;
@@ -529,15 +559,20 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
       t1_hi = n_hi;
       m1 = n_m;
     }
+    const bool rows = ROWS && code == 2;
     for (int r = 0; r < cnt; ++r) {
-      const Reads<SMAX, UCFG> rd = issue_reads<SMAX, UCFG, MB, JPW>(s, cur, li);
+      // the extra-host flag of this request (a ballot) is taken here, at the
+      // top, so that its branch is a scalar one
+      const bool ex = EXTRA && cur.extra();
+      const Reads<SMAX, UCFG> rd = issue_reads<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0>(s, cur, li, ex);
       // the next request, prepared while this one's reads are in flight
       const double t_nx =
           __hiloint2double(__builtin_amdgcn_readlane(t1_hi, r), __builtin_amdgcn_readlane(t1_lo, r));
-      const Plan<MB> nxt = make_plan<MB, EXTRA>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
+      const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
       double out;
-      const bool served = finish_step<SMAX, UCFG, MB, JPW>(s, cur, rd, li, ln.scale, a.C, a.G, S0, active, out);
-      result(cb + r, r, out, served);
+      const bool served = finish_step<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0, FULL>(s, cur, rd, li, ln.scale, a.C,
+                                                                              a.G, S0, active, out);
+      result(cb + r, r, out, served, rows);
       cur = nxt;
     }
     chunk_end(cb, cnt);
@@ -547,32 +582,19 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
 
 __device__ __forceinline__ int spec_ckpts(int64_t b, int64_t e, int64_t ck) { return (int)((e - b - 1) / ck); }
 
-// Pass 0: every (job, segment) from a warmed-up estimate of its start state;
-// the state is also saved every ck requests (checkpoints for the rounds).
-// Every kernel of the speculative pipeline that simulates requests comes in
-// four variants, all launched: UCFG (all groups of all placements share one
-// configuration) and EXTRA (some lane of the wavefront hosts a model on more
-// than two groups) select the code; a workgroup whose data do not match its
-// variant returns at once, before any side effect.
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA>
-__global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
-  if ((a.cfg_info[0] != 0) != UCFG) return;
-  const int c0 = UCFG ? a.cfg_info[1] : 0;
-  extern __shared__ double lds[];
-  const int lane = threadIdx.x;
-  const int jb = blockIdx.x % a.njb;
-  const int k = blockIdx.x / a.njb;
-  const SpecLane ln = spec_lane<JPW>(a, jb, lane);
+// Pass 0 of one wavefront; ROWS: some lane of it writes finish rows.
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL, bool ROWS>
+__device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, int lane, int k,
+                                                const SpecLane& ln, int c0) {
   LaneMasks<MB> msk;
-  const bool many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-  if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
+  (void)msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+  const bool wave_rows = ROWS;
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int GS = a.G * SMAX;
   if (lane < JPW)
     for (int q = 0; q < GS; ++q) s.F[q * JPW + lane] = 0.0;
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   if (blockIdx.x == 0 && lane < a.nseg) a.changed[lane] = lane == 0 ? 1 : 0;
-  const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
 
   const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
   const int64_t J = a.J;
@@ -589,7 +611,7 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   const size_t ck0 = (size_t)k * a.ckps;
   if (w0 == b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA>(
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, FULL, ROWS>(
       a, s, msk, ln, lane, S0, w0, e, on,
       [&](int64_t cb) {
         if (cb == b) {
@@ -606,12 +628,12 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
           a.ck_served[j * J + ln.job] = served;
           a.ck_fsum[j * J + ln.job] = fsum;
         }
-        return true;
+        return rows_now ? 2 : 1;
       },
-      [&](int64_t i, int r, double out, bool sv) {
+      [&](int64_t i, int r, double out, bool sv, bool rows) {
         fsum += sv ? bits_of(out) : 0;
         word = push_bit(word, sv);
-        if (rows_now && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+        if (rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [&](int64_t cb, int cnt) {
         word = chunk_word(word, cnt);
@@ -631,6 +653,38 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   for (int q = 0; q < GS; ++q) a.st_end[seg_base + (size_t)q * J] = s.F[q * JPW + lane];  // buffer 0
   a.seg_served[(size_t)k * J + ln.job] = served;
   a.seg_fsum[(size_t)k * J + ln.job] = fsum;
+}
+
+// Pass 0: every (job, segment) from a warmed-up estimate of its start state;
+// the state is also saved every ck requests (checkpoints for the rounds).
+// Every kernel of the speculative pipeline that simulates requests comes in
+// four variants, all launched: UCFG (all groups of all placements share one
+// configuration) and EXTRA (some lane of the wavefront hosts a model on more
+// than two groups) select the code; a workgroup whose data do not match its
+// variant returns at once, before any side effect.  FULL (every
+// configuration has SMAX stages, so a uniform one runs the whole chain) is
+// chosen on the host.
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
+__global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
+  if ((a.cfg_info[0] != 0) != UCFG) return;
+  const int c0 = UCFG ? a.cfg_info[1] : 0;
+  extern __shared__ double lds[];
+  const int lane = threadIdx.x;
+  const int jb = blockIdx.x % a.njb;
+  const int k = blockIdx.x / a.njb;
+  const SpecLane ln = spec_lane<JPW>(a, jb, lane);
+  {
+    LaneMasks<MB> m0;
+    const bool many = m0.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+    if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
+  }
+  // the wavefronts with finish rows (few) run their own copy of the loop,
+  // so that the others carry no per-request code for the rows
+  if (__builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0) {
+    spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL, true>(a, lds, lane, k, ln, c0);
+  } else {
+    spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL, false>(a, lds, lane, k, ln, c0);
+  }
 }
 
 // Round q >= 1: a segment whose start state differs from its predecessor's
@@ -683,7 +737,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
   bool coupled = false, gave_up = false;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA>(
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, false, true>(
       a, s, msk, ln, lane, S0, b, e, active,
       [&](int64_t cb) {
         if (cb > b && (cb - b) % a.ck == 0 && active) {
@@ -720,14 +774,14 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
           // runs from the two states do not meet: the pipeline gives up
           if (lane == 0) a.cfg_info[2] = 1;
           gave_up = true;
-          return false;
+          return 0;
         }
-        return any;
+        return any ? (wave_rows ? 2 : 1) : 0;
       },
-      [&](int64_t i, int r, double out, bool sv) {
+      [&](int64_t i, int r, double out, bool sv, bool rows) {
         fsum += sv ? bits_of(out) : 0;
         word = push_bit(word, sv);
-        if (wave_rows && ln.frow >= 0 && active) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+        if (rows && ln.frow >= 0 && active) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [&](int64_t cb, int cnt) {
         word = chunk_word(word, cnt);
@@ -1064,13 +1118,27 @@ void spec_rounds_gpl_w(const SpecArgs& a, hipStream_t s) {
   }
 }
 
+// Whether every configuration has SMAX stages: a uniform configuration is
+// then the deepest kind, and pass 0 runs every stage of the chain.
+template <int SMAX>
+bool spec_full(const SpecArgs& a) {
+  for (int c = 0; c < a.C; ++c)
+    if (a.cfg_stages[c] != SMAX) return false;
+  return true;
+}
+
 template <int SMAX, int MB, int JPW>
 hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.njb * a.nseg)), block(64);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false>), grid, block, lds_u, s, a);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true>), grid, block, lds_u, s, a);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, false>), grid, block, lds_g, s, a);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, true>), grid, block, lds_g, s, a);
+  if (spec_full<SMAX>(a)) {
+    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false, true>), grid, block, lds_u, s, a);
+    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true, true>), grid, block, lds_u, s, a);
+  } else {
+    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false, false>), grid, block, lds_u, s, a);
+    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true, false>), grid, block, lds_u, s, a);
+  }
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, false, false>), grid, block, lds_g, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, true, false>), grid, block, lds_g, s, a);
   if (a.G <= 16 && spec_gpl_rounds()) {
     spec_rounds_gpl_w<SMAX>(a, s);
   } else {
@@ -1090,7 +1158,7 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
 template <int SMAX, int MB, int JPW>
 int spec_occupancy(size_t lds) {
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW, false>, 64, lds) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW, false, false>, 64, lds) != hipSuccess)
     return 1;
   return nb > 0 ? nb : 1;
 }
