@@ -130,8 +130,9 @@ def test_c3_candidate_steps_every_partition(gpu):
         compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), len(pb.t), f"c3 p{pi}")
 
 
-def _random_problem(rng, G, S, n, P, K, M=None, mixed=True):
-    """Random problem with exactly G groups, up to S stages, mixed configs."""
+def _random_problem(rng, G, S, n, P, K, M=None, mixed=True, max_hosts=4):
+    """Random problem with exactly G groups, up to S stages, mixed configs;
+    a hosted model has 1..max_hosts hosting groups."""
     from paper_2302_11665_amd.workload.problems import Problem
     M = M or int(rng.integers(1, 9))
     C = int(rng.integers(1, 5)) if mixed else 1
@@ -150,7 +151,7 @@ def _random_problem(rng, G, S, n, P, K, M=None, mixed=True):
         for m in range(M):
             if rng.random() < 0.15:
                 continue  # unhosted model
-            k = int(rng.integers(1, min(G, 4) + 1))
+            k = int(rng.integers(1, min(G, max_hosts) + 1))
             valid = [g for g in range(G) if gcfg[p, g] >= 0]
             for g in rng.choice(valid, size=min(k, len(valid)), replace=False):
                 masks[p, m] = np.uint64(int(masks[p, m]) | (1 << int(g)))
@@ -173,6 +174,23 @@ def test_random_shapes_every_width(gpu, G):
         say("random", G, S, n, P, K)
         res = gpu.simulate_problem(pb)
         compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), n, f"random G={G} S={S} n={n}")
+
+
+@pytest.mark.parametrize("G", [3, 9, 16, 32, 64])
+def test_random_many_hosts(gpu, G):
+    """Models on up to every group: the dispatch over more than two hosts
+    (the further hosts read in one batch, the winning row read again) and
+    over more than eight (the loop past the batch), with unhosted models
+    beside them."""
+    rng = np.random.default_rng(700 + G)
+    for S in (1, 4):
+        for mixed in (False, True):
+            n = int(rng.choice([65, 2049, 5000]))
+            pb = _random_problem(rng, G, S, n, int(rng.integers(1, 24)), 2, M=int(rng.integers(2, 12)),
+                                 mixed=mixed, max_hosts=G)
+            say("many hosts", G, S, n, mixed)
+            res = gpu.simulate_problem(pb)
+            compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), n, f"many hosts G={G} S={S} n={n}")
 
 
 def test_tiny_cases_like_the_brute_force_pins(gpu):
