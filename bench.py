@@ -51,19 +51,19 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "e1ed0330e506a2f23b85389533f900eb7c8f5c7e56ee3e40a5aee5f8ace8a460",
+    "sources_sha256": "7c54cc42d596a65efbd621b1f5b5eaab133d65300741ef36d9b6283489a40f56",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
     "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check "
               "(+ the pass-0 variants that return at once)",
-    "fetch_kib": 2159256.0, "write_kib": 5990874.8125,
+    "fetch_kib": 2158401.5, "write_kib": 5990875.09375,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "e1ed0330e506a2f23b85389533f900eb7c8f5c7e56ee3e40a5aee5f8ace8a460",
+    "sources_sha256": "7c54cc42d596a65efbd621b1f5b5eaab133d65300741ef36d9b6283489a40f56",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595228.75, "write_kib": 13848.96875,
+    "fetch_kib": 2595227.625, "write_kib": 13847.75,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 

@@ -130,7 +130,7 @@ __device__ __forceinline__ uint64_t bits_of(double x) { return (uint64_t)__doubl
 
 // Accept bits of a chunk: each request's bit enters at the top and moves down
 // one place per request, so that after the chunk's cnt requests chunk_word
-// has request r's bit at r.
+// has request r's bit at r (bits pushed before them fall out of the word).
 __device__ __forceinline__ uint64_t push_bit(uint64_t w, bool bit) {
   const uint32_t lo = (uint32_t)w, hi = (uint32_t)(w >> 32);
   return ((uint64_t)__builtin_amdgcn_alignbit((uint32_t)bit, hi, 1) << 32) | __builtin_amdgcn_alignbit(hi, lo, 1);
@@ -527,7 +527,8 @@ struct TraceChunks {
 // lane of the wavefront is active), 1 to run the chunk, 2 to run it with
 // finish rows; result(i, r, out, served, rows) sees every simulated request
 // (on an inactive lane with served false and out meaningless; rows: the chunk
-// writes finish rows), chunk_end(base, cnt) closes the chunk.
+// writes finish rows), after a placeholder call per chunk (i = base - 1,
+// served and rows false), chunk_end(base, cnt) closes the chunk.
 template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL, bool ROWS, class Begin, class Result,
           class End>
 __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
@@ -560,21 +561,27 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
       m1 = n_m;
     }
     const bool rows = ROWS && code == 2;
+    // each request's bookkeeping (result) runs one request late, while the
+    // next request's reads are in flight; the first call of a chunk is a
+    // placeholder (not served: its accept bit is shifted out of the word at
+    // the chunk's end, and it writes no row)
+    double out_p = 0.0;
+    bool served_p = false;
     for (int r = 0; r < cnt; ++r) {
       // the extra-host flag of this request (a ballot) is taken here, at the
       // top, so that its branch is a scalar one
       const bool ex = EXTRA && cur.extra();
       const Reads<SMAX, UCFG> rd = issue_reads<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0>(s, cur, li, ex);
+      result(cb + r - 1, r - 1, out_p, served_p, rows && r > 0);
       // the next request, prepared while this one's reads are in flight
       const double t_nx =
           __hiloint2double(__builtin_amdgcn_readlane(t1_hi, r), __builtin_amdgcn_readlane(t1_lo, r));
       const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
-      double out;
-      const bool served = finish_step<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0, FULL>(s, cur, rd, li, ln.scale, a.C,
-                                                                              a.G, S0, active, out);
-      result(cb + r, r, out, served, rows);
+      served_p = finish_step<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0, FULL>(s, cur, rd, li, ln.scale, a.C, a.G, S0,
+                                                                       active, out_p);
       cur = nxt;
     }
+    result(cb + cnt - 1, cnt - 1, out_p, served_p, rows);
     chunk_end(cb, cnt);
     if (!last_chunk) tc.advance(a, cb + 128, lane);
   }
