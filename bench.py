@@ -51,7 +51,7 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "7c54cc42d596a65efbd621b1f5b5eaab133d65300741ef36d9b6283489a40f56",
+    "sources_sha256": "db23ea9d793d142c29b6625b3b862d972ffca9a72d44fb79f3ce2eca424e9f5f",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
@@ -61,7 +61,7 @@ MEASURED_TRAFFIC = {
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "7c54cc42d596a65efbd621b1f5b5eaab133d65300741ef36d9b6283489a40f56",
+    "sources_sha256": "db23ea9d793d142c29b6625b3b862d972ffca9a72d44fb79f3ce2eca424e9f5f",
     "kernel": "seg_kernel<1>",
     "fetch_kib": 2595227.625, "write_kib": 13847.75,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,

@@ -37,8 +37,10 @@
 // warm-up estimate is usually exact and the rounds re-run little.
 //
 // State layout: F[g][s] of a lane lives in LDS as [g][s][lane] (conflict-free
-// for any per-lane g); each lane's hosting masks live in registers (a uniform
-// model index selects one); arrivals are uniform and read with scalar loads.
+// for any per-lane g), with a spare row that unserved requests write and a
+// sentinel row that stands for a missing host; each lane's hosting masks live
+// in registers (a uniform model index selects one); arrivals come in chunks
+// of 64, one per lane, and a request is read from its lane with readlane.
 //
 // Exactness: the same IEEE operations in the same order as the definition
 // (v_max_f64, single v_add_f64, no FMA), so finish times are bit-identical.
