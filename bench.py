@@ -51,19 +51,19 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "db23ea9d793d142c29b6625b3b862d972ffca9a72d44fb79f3ce2eca424e9f5f",
+    "sources_sha256": "e2ab740cff711c9a95b23ecca30faeef2f2d388fb4842717793cbd699477680d",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
     "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check "
               "(+ the pass-0 variants that return at once)",
-    "fetch_kib": 2158401.5, "write_kib": 5990875.09375,
+    "fetch_kib": 2158277.1875, "write_kib": 5990858.875,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "db23ea9d793d142c29b6625b3b862d972ffca9a72d44fb79f3ce2eca424e9f5f",
+    "sources_sha256": "e2ab740cff711c9a95b23ecca30faeef2f2d388fb4842717793cbd699477680d",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595227.625, "write_kib": 13847.75,
+    "fetch_kib": 2595234.4375, "write_kib": 13848.34375,
     "fetch_scale": 1048576.0 / 524299.625, "write_scale": 1048576.0 / 1048576.0,
 }
 

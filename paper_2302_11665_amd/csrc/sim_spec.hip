@@ -820,6 +820,20 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = E_in[own + (size_t)x * J];
 }
 
+// Unsigned minimum over each aligned group of W <= 16 lanes, in every lane of
+// it: one v_min_u32 with a DPP operand per halving step.  Every lane of the
+// group must be active.
+template <int W>
+__device__ __forceinline__ uint32_t seg_min_u32w(uint32_t x) {
+  static_assert(W <= 16, "row-local steps only");
+  auto umin = [](uint32_t p, uint32_t q) { return p < q ? p : q; };
+  if constexpr (W >= 2) x = umin(x, dpp_u32<kXor1>(x));
+  if constexpr (W >= 4) x = umin(x, dpp_u32<kXor2>(x));
+  if constexpr (W >= 8) x = umin(x, dpp_u32<kHalfMirror>(x));
+  if constexpr (W >= 16) x = umin(x, dpp_u32<kMirror>(x));
+  return x;
+}
+
 // Round q >= 1 in the group-per-lane layout (jobs of at most 16 groups): the
 // same protocol as spec_round, but a job has W lanes, one group each, with its
 // stage free times in registers and the dispatch a DPP min over the W lanes.
@@ -899,7 +913,6 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
   const int nck = b < e ? spec_ckpts(b, e, a.ck) : 0;
   uint64_t served = 0, fsum = 0;  // this lane's share (the requests it committed)
   bool coupled = false;
-  const double kInf = __builtin_inf();
   TraceChunks tc;
   tc.first(a, b, e, lane);
   for (int64_t cb = b; cb < e; cb += 64) {
@@ -960,10 +973,23 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
       double L[SMAX];
 #pragma unroll
       for (int st = 0; st < SMAX; ++st) L[st] = Lt[((size_t)mi * a.C + cg) * SMAX + st];
-      const double key = host ? F[0] : kInf;
-      const double mn = seg_min<W>(key);
-      const bool eq = host && key == mn;
-      const uint64_t ball = __builtin_amdgcn_ballot_w64(eq);
+      // dispatch on the free times' bit patterns: they are >= 0 (the sign
+      // bit cleared merges -0 with +0), so the unsigned order of the patterns
+      // is the numeric order; lanes not hosting m take all ones.  The high
+      // words first, the low words only where two lanes of a job tie on the
+      // high word.  (The cross-lane minima are taken in every lane, never
+      // behind a lane condition: a lane left out would read as zero.)
+      const uint64_t kb = bits_of(F[0]);
+      const uint32_t kh = host ? (uint32_t)(kb >> 32) & 0x7FFFFFFFu : 0xFFFFFFFFu;
+      const uint32_t mh = seg_min_u32w<W>(kh);
+      bool eq = host && kh == mh;
+      uint64_t ball = __builtin_amdgcn_ballot_w64(eq);
+      if (__builtin_amdgcn_ballot_w64(eq && (ball & below) != 0) != 0) {
+        const uint32_t kl = eq ? (uint32_t)kb : 0xFFFFFFFFu;
+        const uint32_t ml = seg_min_u32w<W>(kl);
+        eq = eq && kl == ml;
+        ball = __builtin_amdgcn_ballot_w64(eq);
+      }
       const bool chosen = eq && (ball & below) == 0;
       double f[SMAX];
       double prev = ti;
