@@ -21,10 +21,12 @@ timed the same way, with its HBM roofline (each segment is read once).
 And, as "search": wall time and simulated events of two placement searches
 (reduced and full Alg. 2) on the 32-model / 64-device workload; as
 "batching": the dynamic-batching simulator on the batching experiment's shape
-for maximum batch sizes 1-8.
+for maximum batch sizes 1-8; as "peaks_measured": the fp64 vector and
+device-memory read ceilings measured on this machine, beside the published
+figures the roofline objects use.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep]
-                    [--no-search] [--no-batching]
+                    [--no-search] [--no-batching] [--no-peaks]
 """
 import argparse
 import json
@@ -277,6 +279,33 @@ def bench_batching(args, np, torch, sim, problems):
     return out
 
 
+def measure_peaks(torch):
+    """The two ceilings measured on this machine with the probe library: fp64
+    vector lane-operations per second (v_max_f64 / v_add_f64 chains, the
+    simulator's kind of work) and device-memory read bytes per second over an
+    8 GiB buffer.  Quoted beside the published figures the roofline uses."""
+    import ctypes
+    from paper_2302_11665_amd import build as b
+    if not os.path.exists(b.PROBE_LIB):
+        raise RuntimeError(f"{b.PROBE_LIB} is not built; run __graft_entry__.build()")
+    torch.cuda.synchronize()
+    L = ctypes.CDLL(b.PROBE_LIB)
+    L.as_probe_valu_f64.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    L.as_probe_hbm_read.argtypes = [ctypes.c_size_t, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    ops, bps = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if L.as_probe_valu_f64(cus * 8, 200000, 3, ctypes.byref(ops)) != 0:
+        raise RuntimeError("fp64 VALU probe failed")
+    if L.as_probe_hbm_read(8 << 30, 5, ctypes.byref(bps)) != 0:
+        raise RuntimeError("device-memory read probe failed")
+    return {"fp64_lane_ops_per_s": float(f"{ops.value:.4e}"),
+            "fp64_frac_of_published": round(ops.value / PEAK_FP64_OPS, 4),
+            "hbm_read_bytes_per_s": float(f"{bps.value:.4e}"),
+            "hbm_frac_of_published": round(bps.value / HBM_PEAK, 4),
+            "note": "probes: 8 independent v_max_f64+v_add_f64 chains per lane, "
+                    f"{cus * 8} blocks of 256 threads; 16-byte grid-stride reads of 8 GiB; best of the timed runs"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -289,6 +318,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the SLO-curve sweep workload")
     ap.add_argument("--no-search", action="store_true", help="skip the placement-search timings")
     ap.add_argument("--no-batching", action="store_true", help="skip the dynamic-batching timings")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the fp64 VALU and memory-read peak probes")
     ap.add_argument("--sweep-only", action="store_true",
                     help="time only the SLO-curve sweep (prints its object alone)")
     ap.add_argument("--calibrate-copy", type=float, default=0.0,
@@ -411,6 +441,8 @@ def main():
         out["search"] = bench_search(args, np, torch, sim, problems)
     if not args.no_batching:
         out["batching"] = bench_batching(args, np, torch, sim, problems)
+    if not args.no_peaks:
+        out["peaks_measured"] = measure_peaks(torch)
     print(json.dumps(out), flush=True)
 
 

@@ -2,6 +2,7 @@
 
   libas_gen.so         workload generator (gcc, plain C, host only)
   libalpaserve_sim.so  HIP kernels for gfx950 + C-ABI (hipcc)
+  libas_probe.so       fp64 VALU and device-memory read probes (hipcc; bench.py only)
 
 Both land in paper_2302_11665_amd/_build/.  Every call recompiles.
 """
@@ -28,6 +29,8 @@ SIM_BATCH_SRC = os.path.join(CSRC, "sim_batch.hip")
 SIM_SPEC_SRC = os.path.join(CSRC, "sim_spec.hip")
 LANE_WIDTHS = (1, 2, 4, 8, 16, 32, 64)  # one launcher translation unit per width
 SIM_LIB = os.path.join(BUILD, "libalpaserve_sim.so")
+PROBE_SRC = os.path.join(CSRC, "peak_probe.hip")
+PROBE_LIB = os.path.join(BUILD, "libas_probe.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -87,6 +90,16 @@ def build_sim(extra_flags=(), jobs=None) -> str:
     return SIM_LIB
 
 
+def build_probe() -> str:
+    """The peak probes: a stand-alone library that bench.py loads."""
+    os.makedirs(BUILD, exist_ok=True)
+    tmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-o", tmp, PROBE_SRC])
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
+
+
 def build_all() -> None:
     build_gen()
     build_sim()
+    build_probe()
