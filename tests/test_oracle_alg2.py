@@ -72,6 +72,50 @@ def test_bucket_options():
     assert 3 not in opts5  # 4 devices do not fit in 2
 
 
+def test_bucket_options_remainder_not_deeper_than_the_bucket_configuration():
+    """Hand-derived: the last group of a bucket takes a configuration of the
+    remaining device count whose pipeline is not deeper than the equal groups'
+    one.  Sizes 1, 2, 2, 4, 4 with depths 1, 2, 1, 4, 1."""
+    cfg_devices = np.array([1, 2, 2, 4, 4], np.int32)
+    cfg_stages = np.array([1, 2, 1, 4, 1], np.int32)
+    opts = {c: g.tolist() for c, g, _ in alg2.bucket_options(6, cfg_devices, cfg_stages, 1)}
+    assert opts[4] == [4, 2]  # 4 + 2 at depth 1: the 2-device group is (S=1, k=2), not (S=2, k=1)
+    assert opts[3] == [3, 1]  # 4 + 2 at depth 4: the deepest 2-device pipeline, S=2
+    # depth 1 and no 2-device configuration of depth <= 1: skipped
+    opts_b = {c: g.tolist() for c, g, _ in alg2.bucket_options(6, np.array([2, 4], np.int32),
+                                                                np.array([2, 1], np.int32), 1)}
+    assert 1 not in opts_b and opts_b[0] == [0, 0, 0]
+
+
+def _balance_instance():
+    """Two models of latency 0.5 s with three requests each: every bucket's
+    load is 1.5 s of work divided by its devices (exact in binary)."""
+    t = np.array([0.0, 0.0, 1.0, 1.0, 2.0, 2.0])
+    model = np.array([0, 1, 0, 1, 0, 1], np.int32)
+    d = np.array([0.5, 0.5])
+    cfg_stages = np.array([1], np.int32)
+    L = np.full((2, 1, 1), 0.5)
+    return t, model, d, cfg_stages, L
+
+
+@pytest.mark.parametrize("ratio,kept", [(1.0, 2), (2.0, 2), (2.999, 2), (3.0, 4), (float("inf"), 4)])
+def test_balance_rule_keeps_the_splits_of_similar_load(olib, ratio, kept):
+    """Sec. 4.2 drops device splits whose buckets would work at very different
+    paces.  4 devices, buckets {0}, {1} (threshold 0 keeps equal latencies
+    together or apart): the one-bucket cut has one split (always kept), the
+    two-bucket cut has (1,3), (2,2), (3,1) with per-device loads 1.5 vs 0.5,
+    0.75 vs 0.75 and 0.5 vs 1.5: largest/smallest 3, 1, 3.  Kept iff that
+    ratio <= the balance ratio."""
+    t, model, d, cs, L = _balance_instance()
+    r = alg2.placement_search(olib, t, model, d, np.array([1, 1], np.int64), cs, L, np.array([1], np.int32), 4,
+                              1, 4, 0.0, ratio, 2, 1, 10.0)
+    assert r["n_bucket_configs"] == 2
+    assert r["n_device_splits"] == 4
+    assert r["n_kept_splits"] == kept
+    if ratio < 3.0 and len(r["buckets"]) == 2:
+        assert [b["devices"] for b in r["buckets"]] == [2, 2]
+
+
 def _instance(seed, M, n_dev, duration=8.0):
     rng = np.random.default_rng(seed)
     d = rng.uniform(0.1, 0.5, M)
