@@ -10,7 +10,7 @@ before the timed region.
 
 Prints ONE JSON line: events/s (request x placement pairs per second), the
 roofline of the simulator kernel, and the CPU oracle's rate on a bounded
-sample of the same workload (single thread), with sampled bit-exact parity.
+sample of the same workload (single thread).
 
 Also reported, as "sweep": the SLO-curve sweep workload -- one fixed
 placement (the 32-model / 64-device greedy search's best, 64 single-device
@@ -18,15 +18,22 @@ groups) over a 16 x 16 x 16 grid of rate scale, CV and SLO scale, every grid
 point with its own 10-minute trace (4096 segments, about 4.4e8 requests) --
 timed the same way, with its HBM roofline (each segment is read once).
 
+The oracle's rate is taken on one pinned core (median of 3 runs over a
+sample of jobs), and every job of the heavy trace and of the sweep is then
+recomputed by the oracle on the host's cores and compared ("parity_full").
+As "small_configs": the 4-model tiny case and one 512-job greedy step, timed
+and compared with the oracle on every job.
+
 And, as "search": wall time and simulated events of two placement searches
-(reduced and full Alg. 2) on the 32-model / 64-device workload; as
+(reduced and full Alg. 2) on the 32-model / 64-device workload and of the
+fast heuristic on its 10 uniform partitions beside the greedy's results; as
 "batching": the dynamic-batching simulator on the batching experiment's shape
 for maximum batch sizes 1-8; as "peaks_measured": the fp64 vector and
 device-memory read ceilings measured on this machine, beside the published
 figures the roofline objects use.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-sweep]
-                    [--no-search] [--no-batching] [--no-peaks]
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--cpu-sample J] [--no-cpu] [--no-parity-full]
+                    [--no-small] [--no-sweep] [--no-search] [--no-batching] [--no-peaks]
 """
 import argparse
 import json
@@ -72,6 +79,81 @@ MEASURED_TRAFFIC_SWEEP = {
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def host_threads():
+    """Oracle worker threads: the CPUs this process may run on, at most 16 (a
+    one-GPU share of the host)."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def host_cpu_info():
+    """CPU model, clocks and counts of the host the oracle runs on."""
+    model = mhz = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                k, _, v = line.partition(":")
+                k = k.strip()
+                if k == "model name" and model is None:
+                    model = v.strip()
+                elif k == "cpu MHz" and mhz is None:
+                    mhz = float(v)
+    except (OSError, ValueError):
+        pass
+    max_mhz = None
+    try:
+        with open("/sys/devices/system/cpu/cpu0/cpufreq/cpuinfo_max_freq") as f:
+            max_mhz = int(f.read().strip()) / 1000.0
+    except (OSError, ValueError):
+        pass
+    return {"cpu_model": model, "cpu_mhz": mhz, "cpu_max_mhz": max_mhz, "nproc": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0))}
+
+
+def oracle_cpu_baseline(lib, N, jobs, one_job, runs=3):
+    """The oracle as it stands, single-threaded and pinned to one core: the
+    same jobs `runs` times, the median run's events/s."""
+    cpus = sorted(os.sched_getaffinity(0))
+    core = cpus[0]
+    os.sched_setaffinity(0, {core})
+    times = []
+    try:
+        for r in range(runs):
+            t0 = time.perf_counter()
+            for j in jobs:
+                one_job(j)
+            times.append(time.perf_counter() - t0)
+            log(f"cpu oracle run {r + 1}/{runs}: {len(jobs)} jobs in {times[-1]:.2f}s")
+    finally:
+        os.sched_setaffinity(0, set(cpus))
+    med = sorted(times)[len(times) // 2]
+    return {"value": round(len(jobs) * N / med, 1), "unit": "events/s", "cores": 1, "kind": "oracle",
+            "pinned_core": core, "runs_s": [round(x, 3) for x in times], "statistic": f"median of {runs} runs",
+            **host_cpu_info()}
+
+
+def oracle_parity_full(jobs, one_job, check, label):
+    """Every job recomputed by the oracle on host_threads() threads (the
+    oracle's C calls release the GIL) and compared by check(j, result), which
+    returns the number of mismatching fields."""
+    from concurrent.futures import ThreadPoolExecutor
+    nthreads = host_threads()
+    jobs = list(jobs)
+    mism, bad = 0, []
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(nthreads) as ex:
+        for q, (j, r) in enumerate(zip(jobs, ex.map(one_job, jobs))):
+            k = check(j, r)
+            if k:
+                mism += k
+                if len(bad) < 8:
+                    bad.append(int(j))
+            if (q + 1) % 1024 == 0 or q + 1 == len(jobs):
+                log(f"{label} full parity: {q + 1}/{len(jobs)} jobs, {mism} mismatches, "
+                    f"{time.perf_counter() - t0:.1f}s")
+    return {"jobs": len(jobs), "mismatches": mism, "first_bad_jobs": bad, "cores": nthreads,
+            "wall_s": round(time.perf_counter() - t0, 2), "kind": "oracle, every job"}
 
 
 def algorithmic_ops(pb):
@@ -168,6 +250,31 @@ def bench_sweep(args, np, torch, api, problems):
     res = api.sweep_results(ds)
     del ds
     torch.cuda.empty_cache()
+    parity = None
+    if not args.no_cpu:
+        import oracle
+        lib = oracle.lib()
+        lens = np.diff(sp.seg_offsets)
+        fset = set(int(x) for x in sp.finish_jobs)
+
+        def one(j):
+            s = int(sp.job_segment[j])
+            a, b = int(sp.seg_offsets[s]), int(sp.seg_offsets[s + 1])
+            return lib.simulate_job(sp.t[a:b], sp.model[a:b], sp.d_single, sp.cfg_stages, sp.stage_lat,
+                                    sp.group_cfg[sp.job_placement[j]], sp.host_mask[sp.job_placement[j]],
+                                    sp.job_scale[j], want_finish=j in fset)
+
+        def check(j, r):
+            s, dg, fin = r
+            n = int(lens[sp.job_segment[j]])
+            bad = int(int(res["served"][j]) != s) + int(tuple(int(x) for x in res["digest"][j]) != dg)
+            bad += int(res["attain"][j] != (s / n if n else 0.0))
+            if fin is not None:
+                bad += int(res["finish"][j][:n].tobytes() != fin.tobytes())
+            return bad
+
+        parity = oracle_parity_full(range(len(sp.job_segment)), one, check, "sweep")
+        parity["finish_rows"] = len(fset)
     return {"workload": "SLO-curve sweep: 32 models, 64 single-device groups (greedy best), 16x16x16 grid of "
                         "rate scale x CV x SLO scale, own 600 s trace per point",
             "jobs": int(len(sp.job_segment)), "requests": int(len(sp.t)), "events": int(events),
@@ -175,8 +282,58 @@ def bench_sweep(args, np, torch, api, problems):
             "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                          "frac": round(gbs * 1e9 / HBM_PEAK, 5), "traffic": measured_traffic(MEASURED_TRAFFIC_SWEEP, True),
                          "algorithmic_bytes": int(nbytes)},
-            "served_total": int(res["served"].sum()),
+            "served_total": int(res["served"].sum()), "parity_full": parity,
             "trace_gen_s": round(gen_s, 3), "upload_s": round(up_s, 3)}
+
+
+def bench_small(args, np, torch, api, problems):
+    """The two small configurations: the 4-model tiny case (all 273 maps of 4
+    models onto the partitions of 4 devices, Poisson 5 req/s per model, 60 s,
+    SLO scale 5) and one greedy step of the 16-model case (64 single-replica
+    candidates x 8 SLO scales, Gamma 4 req/s per model CV 3, 10 minutes).
+    Each call timed with HIP events (mean of 20 after 3 warm-ups); every job
+    compared with the oracle; the oracle's single-core rate over all jobs."""
+    out = {}
+    lib = None
+    if not args.no_cpu:
+        import oracle
+        lib = oracle.lib()
+    for name, pb in (("tiny_273_jobs", problems.c1_tiny()), ("greedy_step_512_jobs", problems.c2_greedy_step())):
+        N, J, K = len(pb.t), pb.n_jobs, len(pb.slo_scale)
+        dp = api.upload(pb, finish=False)
+        for _ in range(3):
+            api.run(dp)
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(21)]
+        ev[0].record(stream)
+        for k in range(20):
+            api.run(dp)
+            ev[k + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.mean([ev[k].elapsed_time(ev[k + 1]) for k in range(20)]))
+        res = api.results(dp)
+        rec = {"requests": N, "jobs": J, "events": N * J, "ms_per_call": round(ms, 4),
+               "value": round(N * J / (ms / 1000.0), 1), "unit": "events/s"}
+        if lib is not None:
+            def one(j, pb=pb, K=K):
+                p, k = divmod(int(j), K)
+                return lib.simulate_job(pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat, pb.group_cfg[p],
+                                        pb.host_mask[p], pb.slo_scale[k])
+
+            def check(j, r, res=res, N=N):
+                s, dg, _ = r
+                return (int(int(res["served"][j]) != s) + int(tuple(int(x) for x in res["digest"][j]) != dg)
+                        + int(res["attain"][j] != (s / N if N else 0.0)))
+
+            rec["parity_full"] = oracle_parity_full(range(J), one, check, name)
+            cb = oracle_cpu_baseline(lib, N, list(range(J)), one)
+            rec["cpu_oracle_events_per_s"] = cb["value"]
+            rec["speedup_vs_cpu_oracle"] = round(rec["value"] / cb["value"], 1)
+        log(f"{name}: {ms:.3f} ms/call, {rec['value']:.3e} events/s")
+        out[name] = rec
+        del dp
+    return out
 
 
 def bench_search(args, np, torch, sim, problems):
@@ -219,6 +376,26 @@ def bench_search(args, np, torch, sim, problems):
             res["parity"] = r["served"] == fx["best_served"]
         log(f"search {name}: {wall:.2f}s, {r['launches']} launches, {r['jobs_simulated']} jobs, served {r['served']}")
         out[name] = res
+    # the fast heuristic of Sec. 4.2 on each uniform partition, next to Alg. 1
+    # (beam 1) on the same partition (the oracle's stored result, which the
+    # native greedy search reproduces step for step)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    fast = [sim.as_fast_placement(t, m, ds, gp.cfg_stages, L, gp.weight_mib, part["group_cfg"],
+                                  part["group_mem_mib"], gp.slo_scale) for part in gp.partitions]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fs = [r["best_served"] for r in fast]
+    gs = [p["best_served"] for p in fx["partitions"]]
+    sims = sum(r["n_steps"] + 1 for r in fast)
+    out["fast_heuristic"] = {
+        "wall_s": round(wall, 3), "simulations": sims, "events": sims * N,
+        "served_by_partition": fs, "greedy_served_by_partition": gs,
+        "ratio_by_partition": [round(a / b, 5) if b else None for a, b in zip(fs, gs)],
+        "best_served": max(fs), "greedy_best_served": max(gs),
+        "ratio_best": round(max(fs) / max(gs), 5) if max(gs) else None,
+        "note": "Sec. 4.2 expects the heuristic's attainment at >= 98% of the greedy search's"}
+    log(f"search fast heuristic: {wall:.2f}s, {sims} simulations, best {max(fs)} vs greedy {max(gs)}")
     return out
 
 
@@ -313,8 +490,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--placements", type=int, default=8192)
     ap.add_argument("--duration", type=float, default=3600.0)
-    ap.add_argument("--cpu-sample", type=int, default=192, help="jobs timed on the CPU oracle")
-    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=64,
+                    help="jobs timed on the CPU oracle (single core, median of 3 runs)")
+    ap.add_argument("--no-cpu", action="store_true", help="no oracle work at all (baseline and parity)")
+    ap.add_argument("--no-parity-full", action="store_true",
+                    help="skip the every-job oracle comparison of the heavy-trace step")
+    ap.add_argument("--no-small", action="store_true", help="skip the two small configurations")
     ap.add_argument("--no-sweep", action="store_true", help="skip the SLO-curve sweep workload")
     ap.add_argument("--no-search", action="store_true", help="skip the placement-search timings")
     ap.add_argument("--no-batching", action="store_true", help="skip the dynamic-batching timings")
@@ -404,35 +585,39 @@ def main():
                       "finish_jobs": int(len(pb.finish_jobs))},
            "roofline": roof, "trace_gen_s": round(gen_s, 3), "upload_s": round(up_s, 3)}
 
-    if not args.no_cpu and args.cpu_sample > 0:
+    if not args.no_cpu:
         import oracle
         if not os.path.exists(oracle.LIB_PATH):
             oracle.build()
         lib = oracle.lib()
-        step = max(1, J // args.cpu_sample)
-        sample = list(range(0, J, step))[: args.cpu_sample]
-        fset = set(int(x) for x in pb.finish_jobs[:2])
-        mism = 0
-        t0 = time.perf_counter()
-        for q, j in enumerate(sample):
-            s, dg, fin = lib.simulate_job(pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat,
-                                          pb.group_cfg[j], pb.host_mask[j], pb.slo_scale[0],
-                                          want_finish=j in fset)
-            if int(res["served"][j]) != s or tuple(int(x) for x in res["digest"][j]) != dg:
-                mism += 1
-            if fin is not None and res["finish"][j].tobytes() != fin.tobytes():
-                mism += 1
-            if q % 16 == 15:
-                log(f"cpu oracle {q + 1}/{len(sample)} jobs")
-        cpu_s = time.perf_counter() - t0
-        # the parity comparisons above are outside the oracle's own work but
-        # negligible next to it
-        cpu_rate = len(sample) * N / cpu_s
-        out["cpu_baseline"] = {"value": round(cpu_rate, 1), "unit": "events/s", "cores": 1, "kind": "oracle",
-                               "sample": f"{len(sample)} of {J} jobs (every {step}th) x full trace = "
-                                         f"{len(sample) * N:.3e} events, single thread, {cpu_s:.1f}s"}
-        out["parity_sampled"] = {"jobs": len(sample), "finish_rows": len(fset), "mismatches": mism}
-        out["speedup_vs_cpu_oracle"] = round(value / cpu_rate, 1)
+        fset = set(int(x) for x in pb.finish_jobs)
+
+        def one(j, finish=True):
+            return lib.simulate_job(pb.t, pb.model, pb.d_single, pb.cfg_stages, pb.stage_lat, pb.group_cfg[j],
+                                    pb.host_mask[j], pb.slo_scale[0], want_finish=finish and j in fset)
+
+        def check(j, r):
+            s, dg, fin = r
+            bad = int(int(res["served"][j]) != s) + int(tuple(int(x) for x in res["digest"][j]) != dg)
+            bad += int(res["attain"][j] != s / N)
+            if fin is not None:
+                bad += int(res["finish"][j].tobytes() != fin.tobytes())
+            return bad
+
+        if args.cpu_sample > 0:
+            step = max(1, J // args.cpu_sample)
+            sample = list(range(0, J, step))[: args.cpu_sample]
+            cb = oracle_cpu_baseline(lib, N, sample, lambda j: one(j, False))
+            cb["sample"] = (f"{len(sample)} of {J} jobs (every {step}th) x the full trace = {len(sample) * N:.3e} "
+                            f"events per run, one thread pinned to one core")
+            out["cpu_baseline"] = cb
+            out["speedup_vs_cpu_oracle"] = round(value / cb["value"], 1)
+        if not args.no_parity_full:
+            pf = oracle_parity_full(range(J), one, check, "heavy trace")
+            pf["finish_rows"] = len(fset)
+            out["parity_full"] = pf
+    if not args.no_small:
+        out["small_configs"] = bench_small(args, np, torch, api, problems)
     if not args.no_sweep:
         del dp
         torch.cuda.empty_cache()

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -382,18 +383,24 @@ int run_trace_kernels(KArgs& a, int W, int smax, hipStream_t stream, bool only_c
 // up (traffic under which runs from different states do not meet), the
 // kernels above, launched behind them and gated on that flag, produce the
 // results instead.  All of it stays stream-ordered: no host synchronisation.
-int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream) {
+// A workspace allocation that fails leaves the call to those kernels where
+// they can take it (they need no workspace).  With scratch, the speculative
+// workspace comes from it (nothing is allocated), and a call that needs more
+// than scratch_bytes returns AS_E_LIMITS.
+int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream, void* scratch, size_t scratch_bytes) {
   if (want_spec(a, smax)) {
     const bool fallback = run_trace_kernels(a, W, smax, stream, true) == AS_OK;
     void* ws = nullptr;
     const int32_t* gave_up = nullptr;
-    const int rc = run_spec(a, smax, stream, fallback, &ws, &gave_up);
+    int rc = run_spec(a, smax, stream, fallback, scratch, scratch_bytes, &ws, &gave_up);
+    if (rc == kSpecScratchTooSmall) return AS_E_LIMITS;
+    if (rc == AS_E_NOMEM && fallback) rc = AS_E_LIMITS;
     if (rc != AS_E_LIMITS) {
       if (rc != AS_OK || !fallback) return rc;
       a.gate = gave_up;
       const int rc2 = run_trace_kernels(a, W, smax, stream, false);
       a.gate = nullptr;
-      const hipError_t ef = hipFreeAsync(ws, stream);
+      const hipError_t ef = ws ? hipFreeAsync(ws, stream) : hipSuccess;
       if (rc2 != AS_OK) return rc2;
       if (ef != hipSuccess) return fail(AS_E_HIP, "workspace release failed: %s", hipGetErrorString(ef));
       return ok();
@@ -412,11 +419,16 @@ const char* as_last_error(void) { return g_err.c_str(); }
 
 const char* as_version(void) { return "alpaserve_sim 0.1 gfx950"; }
 
-int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
-                           const as_placements_t* placements, const double* slo_scale,
-                           int32_t n_scales, int64_t* out_served, double* out_attain,
-                           uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
-                           double* out_finish, void* stream) {
+}  // extern "C"
+
+namespace as_host {
+namespace {
+
+// Body of as_simulate_placements.
+int simulate_placements(const as_trace_t* trace, const as_models_t* models,
+                        const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
+                        int64_t* out_served, double* out_attain, uint64_t* out_digest,
+                        const int32_t* finish_jobs, int32_t n_finish, double* out_finish, void* stream) {
   KArgs a;
   std::memset(&a, 0, sizeof a);
   if (!trace) return fail(AS_E_INVALID_ARG, "trace must not be NULL");
@@ -445,6 +457,20 @@ int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
   a.out_digest = out_digest;
   a.finish_stride = trace->n;
   return run_shared_trace(a, W, smax, (hipStream_t)stream);
+}
+
+}  // namespace
+}  // namespace as_host
+
+extern "C" {
+
+int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
+                           const as_placements_t* placements, const double* slo_scale,
+                           int32_t n_scales, int64_t* out_served, double* out_attain,
+                           uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
+                           double* out_finish, void* stream) {
+  return simulate_placements(trace, models, placements, slo_scale, n_scales, out_served, out_attain,
+                             out_digest, finish_jobs, n_finish, out_finish, stream);
 }
 
 int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,

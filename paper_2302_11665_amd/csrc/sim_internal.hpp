@@ -24,8 +24,12 @@ size_t shared_lds_limit();
 // group count in W and the padded stage count in smax.
 int check_common(const as_models_t* models, const as_placements_t* plc, KArgs& a, int& W, int& smax);
 // Launch the batched simulation of a shared trace; a is complete except for
-// the kernel shape, W is the group count on entry.
-int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream);
+// the kernel shape, W is the group count on entry.  With scratch (device
+// memory of scratch_bytes), the speculative kernels take their workspace
+// from it and nothing is allocated; a call that would need more returns
+// AS_E_LIMITS without launching.
+int run_shared_trace(KArgs& a, int W, int smax, hipStream_t stream, void* scratch = nullptr,
+                     size_t scratch_bytes = 0);
 // Statistics launch of the shared-trace kernel (one SLO scale, no per-request
 // output rows); returns AS_E_LIMITS without launching when that kernel cannot
 // take the call (several scales, output rows, tables beyond the LDS).
@@ -40,8 +44,14 @@ int run_shared_stats(KArgs& a, int smax, hipStream_t stream);
 // caller then launches other kernels gated on it, which produce all results,
 // and releases *workspace (stream-ordered, hipFreeAsync) after them.  Without
 // it the workspace is released here and *gave_up is null.
-int run_spec(KArgs& a, int smax, hipStream_t stream, bool can_give_up, void** workspace,
-             const int32_t** gave_up);
+// With caller_ws the workspace is carved from that device memory
+// (caller_ws_bytes long) instead of being allocated, *workspace stays null,
+// and a call that needs more returns kSpecScratchTooSmall (message set,
+// nothing launched).
+int run_spec(KArgs& a, int smax, hipStream_t stream, bool can_give_up, void* caller_ws,
+             size_t caller_ws_bytes, void** workspace, const int32_t** gave_up);
+// run_spec's return when a caller-given workspace is too small (internal).
+constexpr int kSpecScratchTooSmall = -100;
 // Whether a shared-trace call takes the segment-speculative kernels.
 bool want_spec(const KArgs& a, int smax);
 // Whether ALPASERVE_PATH=spec forces them (even with a single segment).

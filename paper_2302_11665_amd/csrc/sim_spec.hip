@@ -50,6 +50,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <type_traits>
 
 #include "alpaserve_sim.h"
@@ -1228,18 +1229,39 @@ int compute_units() {
   return cache[dev];
 }
 
-// Keep freed stream-ordered allocations in the device's pool (the workspace
-// of one call is reused by the next instead of going back to the driver).
-void keep_pool_memory() {
-  static bool done[64] = {false};
+// Stream-ordered workspace allocation from a memory pool private to this
+// library, one per device, whose release threshold is at its maximum: the
+// workspace freed by one call is reused by the next instead of going back to
+// the driver, and the process's default pool keeps its own settings.  Where a
+// private pool cannot be created, the default pool serves as it is.
+hipError_t spec_alloc(void** p, size_t bytes, hipStream_t s) {
+  static std::mutex mu;
+  static hipMemPool_t pools[64];
+  static int state[64] = {0};  // 0 not tried, 1 private pool, 2 default pool
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64 || done[dev]) return;
-  hipMemPool_t pool;
-  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-    uint64_t thr = UINT64_MAX;
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipMallocAsync(p, bytes, s);
+  int st = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (state[dev] == 0) {
+      hipMemPoolProps props;
+      std::memset(&props, 0, sizeof props);
+      props.allocType = hipMemAllocationTypePinned;
+      props.handleTypes = hipMemHandleTypeNone;
+      props.location.type = hipMemLocationTypeDevice;
+      props.location.id = dev;
+      state[dev] = 2;
+      if (hipMemPoolCreate(&pools[dev], &props) == hipSuccess) {
+        uint64_t thr = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pools[dev], hipMemPoolAttrReleaseThreshold, &thr);
+        state[dev] = 1;
+      } else {
+        (void)hipGetLastError();
+      }
+    }
+    st = state[dev];
   }
-  done[dev] = true;
+  return st == 1 ? hipMallocFromPoolAsync(p, bytes, pools[dev], s) : hipMallocAsync(p, bytes, s);
 }
 
 // warm-up requests before a segment (measured on the 8192-placement workload:
@@ -1296,8 +1318,8 @@ bool spec_pays(const KArgs& k, int nseg, int jpw, int per_cu) {
 // ALPASERVE_PATH=spec forces the kernels), or when the workspace would be too
 // large.  With can_give_up the workspace outlives the call: the caller's
 // gated fallback kernels read the give-up flag in it, then release it.
-int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void** workspace,
-             const int32_t** gave_up) {
+int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void* caller_ws,
+             size_t caller_ws_bytes, void** workspace, const int32_t** gave_up) {
   using namespace as_dev;
   *workspace = nullptr;
   *gave_up = nullptr;
@@ -1362,15 +1384,26 @@ int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void** wo
   auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t total = up(b_bitmap) + up(b_state) + up(2 * b_state) + 2 * up(b_seg) + up(b_ckpt) +
                        2 * up(b_cks) + up(b_small);
-  // a workspace beyond a quarter of the device's memory leaves the call to
-  // the kernels that need none
-  size_t free_b = 0, total_b = 0;
-  if (hipMemGetInfo(&free_b, &total_b) != hipSuccess || total > total_b / 4) return AS_E_LIMITS;
-  keep_pool_memory();
   char* ws = nullptr;
-  hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), total, stream);
-  if (e != hipSuccess || !ws)
-    return fail(AS_E_NOMEM, "workspace of %zu bytes: %s", total, hipGetErrorString(e));
+  hipError_t e = hipSuccess;
+  if (caller_ws) {
+    if (total > caller_ws_bytes) {
+      fail(AS_E_LIMITS,
+           "this call needs %zu bytes of speculative-kernel workspace, more than the %zu-byte "
+           "no-allocation scratch; as_simulate_placements takes it",
+           total, caller_ws_bytes);
+      return kSpecScratchTooSmall;
+    }
+    ws = static_cast<char*>(caller_ws);
+  } else {
+    // a workspace beyond a quarter of the device's memory leaves the call to
+    // the kernels that need none
+    size_t free_b = 0, total_b = 0;
+    if (hipMemGetInfo(&free_b, &total_b) != hipSuccess || total > total_b / 4) return AS_E_LIMITS;
+    e = spec_alloc(reinterpret_cast<void**>(&ws), total, stream);
+    if (e != hipSuccess || !ws)
+      return fail(AS_E_NOMEM, "workspace of %zu bytes: %s", total, hipGetErrorString(e));
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     char* p = ws + off;
@@ -1398,12 +1431,12 @@ int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void** wo
     default: e = spec_launch_mb<8>(k.G, a, lds_u, lds_g, stream); break;
   }
   if (e != hipSuccess || !can_give_up) {
-    const hipError_t ef = hipFreeAsync(ws, stream);
+    const hipError_t ef = caller_ws ? hipSuccess : hipFreeAsync(ws, stream);
     if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     if (ef != hipSuccess) return fail(AS_E_HIP, "workspace release failed: %s", hipGetErrorString(ef));
     return ok();
   }
-  *workspace = ws;
+  *workspace = caller_ws ? nullptr : ws;
   *gave_up = a.cfg_info + 2;
   return ok();
 }

@@ -180,7 +180,7 @@ def make_placements(group_cfg, host_mask):
 
 def as_simulate_placements(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
                            slo_scale, out_served, out_attain=None, out_digest=None,
-                           finish_jobs=None, out_finish=None, stream=None):
+                           finish_jobs=None, out_finish=None, stream=None, _fn=None):
     """Marshal to as_simulate_placements.  Device tensors: t[N] f64, model[N] i32,
     d_single[M] f64, stage_lat[M,C,Smax] f64, group_cfg[P,G] i32, host_mask[P,M]
     (int64 storage of the uint64 bitmaps), slo_scale[K] f64, out_served[P*K] i64,
@@ -191,7 +191,8 @@ def as_simulate_placements(t, model, d_single, cfg_stages, stage_lat, group_cfg,
     pl = make_placements(group_cfg, host_mask)
     fj = None if finish_jobs is None else np.ascontiguousarray(finish_jobs, dtype=np.int32)
     nf = 0 if fj is None else int(fj.shape[0])
-    rc = lib().as_simulate_placements(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl),
+    fn = _fn if _fn is not None else lib().as_simulate_placements
+    rc = fn(ctypes.byref(tr), ctypes.byref(md), ctypes.byref(pl),
                                       _ptr(slo_scale), int(slo_scale.shape[0]), _ptr(out_served),
                                       _ptr(out_attain), _ptr(out_digest), _ptr(fj), nf,
                                       _ptr(out_finish), _stream(stream))

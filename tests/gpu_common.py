@@ -4,6 +4,7 @@ element by element (bit-exact: served counts, digests, attain = served / n,
 per-request finish times)."""
 from __future__ import annotations
 
+import os
 import sys
 
 import numpy as np
@@ -14,6 +15,11 @@ import oracle
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+def host_threads():
+    """Oracle worker threads: this process's CPUs, at most 16."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
 
 
 def oracle_problem(pb, jobs=None, finish_jobs=()):
@@ -33,7 +39,7 @@ def oracle_problem(pb, jobs=None, finish_jobs=()):
                                         pb.group_cfg[p], pb.host_mask[p], pb.slo_scale[k],
                                         want_finish=int(j) in want)
 
-    with ThreadPoolExecutor(8) as ex:
+    with ThreadPoolExecutor(host_threads()) as ex:
         for j, r in ex.map(one, list(jobs)):
             out[j] = r
     return out

@@ -267,16 +267,22 @@ def test_validate_catches_bad_data(gpu_api):
 
 def test_c4_full_size_sampled(gpu_api):
     """The benchmark workload at full size (8192 placements x 3.6 M requests) in
-    the benchmark's launch configuration; the oracle recomputes a sample of
-    jobs and two of the per-request output rows."""
+    the benchmark's launch configuration; the oracle recomputes 4 jobs of every
+    block of 64 consecutive jobs (a wavefront's jobs on the speculative
+    kernels, 512 in all, each over the whole trace) and all 16 per-request
+    output rows."""
     from paper_2302_11665_amd.workload import problems
     pb = problems.c4_heavy()
     say("c4 full", pb.n_jobs, len(pb.t))
     res = gpu_api.simulate_problem(pb)
     rng = np.random.default_rng(44)
-    jobs = sorted(set(rng.choice(pb.n_jobs, 6, replace=False).tolist()) | {int(pb.finish_jobs[0]),
-                                                                           int(pb.finish_jobs[-1])})
-    fins = [int(pb.finish_jobs[0]), int(pb.finish_jobs[-1])]
+    jobs = set()
+    for b in range(0, pb.n_jobs, 64):
+        jobs |= set((b + rng.choice(min(64, pb.n_jobs - b), 4, replace=False)).tolist())
+    fins = [int(x) for x in pb.finish_jobs]
+    jobs = sorted(jobs | set(fins))
+    assert len(jobs) >= 512
+    say("c4 full: oracle on", len(jobs), "jobs")
     compare(res, oracle_problem(pb, jobs=jobs, finish_jobs=fins), len(pb.t), "c4 full sampled")
 
 
