@@ -108,6 +108,31 @@ int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
                            uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
                            double* out_finish, void* stream);
 
+/* Bytes of device memory that as_simulate_placements_noalloc may use. */
+#define AS_NOALLOC_SCRATCH_BYTES (256u << 20)
+
+/*
+ * as_simulate_placements for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, hosts that forbid
+ * allocation): the same arguments, kernels and results, bit for bit, but no
+ * hipMalloc, hipFree or other allocating call is made.  Where the speculative
+ * kernels take the call (long traces), their workspace (accept bits and saved
+ * states, about 0.19 bytes per request x job) comes from an array of
+ * AS_NOALLOC_SCRATCH_BYTES in device memory that the library holds on every
+ * device it runs on until the process ends; a call whose workspace would be
+ * larger returns AS_E_LIMITS without launching anything (as_simulate_placements
+ * takes such calls).  Every call on one device shares that device's array, and
+ * the array keeps the last call's contents (each call initialises what it
+ * reads), so calls that overlap on one device -- on different streams, or
+ * from different threads without ordering -- race and give unspecified
+ * results; calls ordered on one stream do not.
+ */
+int as_simulate_placements_noalloc(const as_trace_t* trace, const as_models_t* models,
+                                   const as_placements_t* placements, const double* slo_scale,
+                                   int32_t n_scales, int64_t* out_served, double* out_attain,
+                                   uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
+                                   double* out_finish, void* stream);
+
 /* A job of the segmented variant. */
 typedef struct {
   int32_t placement; /* index into the placements                       */

@@ -424,11 +424,42 @@ const char* as_version(void) { return "alpaserve_sim 0.1 gfx950"; }
 namespace as_host {
 namespace {
 
-// Body of as_simulate_placements.
+// Workspace of as_simulate_placements_noalloc: one array per device, held
+// until the process ends, shared by every call on that device.
+static __device__ __align__(256) unsigned char scratch[AS_NOALLOC_SCRATCH_BYTES];
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept; null with a message set when
+// the lookup fails.  In host code the array's name is only a stand-in for
+// the symbol, never a device address.
+void* scratch_ptr() {
+  static std::mutex mu;
+  static void* ptrs[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    fail(AS_E_HIP, "no current HIP device");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      fail(AS_E_HIP, "scratch address on device %d: %s", dev, hipGetErrorString(e));
+      return nullptr;
+    }
+    ptrs[dev] = p;
+  }
+  return ptrs[dev];
+}
+
+// Body of as_simulate_placements; with no_alloc, the speculative kernels'
+// workspace comes from `scratch` and nothing is allocated.
 int simulate_placements(const as_trace_t* trace, const as_models_t* models,
                         const as_placements_t* placements, const double* slo_scale, int32_t n_scales,
                         int64_t* out_served, double* out_attain, uint64_t* out_digest,
-                        const int32_t* finish_jobs, int32_t n_finish, double* out_finish, void* stream) {
+                        const int32_t* finish_jobs, int32_t n_finish, double* out_finish, void* stream,
+                        bool no_alloc) {
   KArgs a;
   std::memset(&a, 0, sizeof a);
   if (!trace) return fail(AS_E_INVALID_ARG, "trace must not be NULL");
@@ -456,7 +487,10 @@ int simulate_placements(const as_trace_t* trace, const as_models_t* models,
   a.out_attain = out_attain;
   a.out_digest = out_digest;
   a.finish_stride = trace->n;
-  return run_shared_trace(a, W, smax, (hipStream_t)stream);
+  if (!no_alloc) return run_shared_trace(a, W, smax, (hipStream_t)stream);
+  void* ws = scratch_ptr();
+  if (!ws) return AS_E_HIP;
+  return run_shared_trace(a, W, smax, (hipStream_t)stream, ws, AS_NOALLOC_SCRATCH_BYTES);
 }
 
 }  // namespace
@@ -470,7 +504,16 @@ int as_simulate_placements(const as_trace_t* trace, const as_models_t* models,
                            uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
                            double* out_finish, void* stream) {
   return simulate_placements(trace, models, placements, slo_scale, n_scales, out_served, out_attain,
-                             out_digest, finish_jobs, n_finish, out_finish, stream);
+                             out_digest, finish_jobs, n_finish, out_finish, stream, false);
+}
+
+int as_simulate_placements_noalloc(const as_trace_t* trace, const as_models_t* models,
+                                   const as_placements_t* placements, const double* slo_scale,
+                                   int32_t n_scales, int64_t* out_served, double* out_attain,
+                                   uint64_t* out_digest, const int32_t* finish_jobs, int32_t n_finish,
+                                   double* out_finish, void* stream) {
+  return simulate_placements(trace, models, placements, slo_scale, n_scales, out_served, out_attain,
+                             out_digest, finish_jobs, n_finish, out_finish, stream, true);
 }
 
 int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,

@@ -95,6 +95,8 @@ def lib():
                                              ctypes.POINTER(as_placements_t), _P, ctypes.c_int32,
                                              _P, _P, _P, _P, ctypes.c_int32, _P, _P]
         L.as_simulate_placements.restype = ctypes.c_int
+        L.as_simulate_placements_noalloc.argtypes = L.as_simulate_placements.argtypes
+        L.as_simulate_placements_noalloc.restype = ctypes.c_int
         L.as_simulate_jobs.argtypes = [_P, _P, _P, ctypes.c_int32, ctypes.POINTER(as_models_t),
                                        ctypes.POINTER(as_placements_t), _P, ctypes.c_int32, _P, _P, _P,
                                        _P, ctypes.c_int32, _P, ctypes.c_int64, _P]
@@ -176,6 +178,16 @@ def make_models(d_single, cfg_stages: np.ndarray, stage_lat):
 def make_placements(group_cfg, host_mask):
     P, G = group_cfg.shape
     return as_placements_t(P, G, _ptr(group_cfg), _ptr(host_mask))
+
+
+def as_simulate_placements_noalloc(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
+                                   slo_scale, out_served, out_attain=None, out_digest=None,
+                                   finish_jobs=None, out_finish=None, stream=None):
+    """Marshal to as_simulate_placements_noalloc (arguments as for
+    as_simulate_placements; the library allocates nothing)."""
+    return as_simulate_placements(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
+                                  out_served, out_attain, out_digest, finish_jobs, out_finish, stream,
+                                  _fn=lib().as_simulate_placements_noalloc)
 
 
 def as_simulate_placements(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask,
