@@ -141,8 +141,11 @@ typedef struct {
 } as_job_t;
 
 /*
- * Jobs that each bring their own trace segment (SLO-curve sweeps: one
- * placement over many generated workloads).  Segment s is requests
+ * Jobs that each bring their own trace segment: the same simulation (Sec.
+ * 4.3, Sec. 3.2, Sec. 3.4) per job, for the SLO-attainment curves of Sec. 3.2
+ * and Sec. 6 that vary the SLO scale, the rate and the burstiness (CV) of the
+ * workload for one placement, each grid point with its own generated
+ * workload.  Segment s is requests
  * [seg_offsets[s], seg_offsets[s+1]) of t/model, each segment nondecreasing in
  * t on its own.
  *   t, model         concatenated segments (device)
