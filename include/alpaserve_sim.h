@@ -316,11 +316,14 @@ int as_simulate_stats(const as_trace_t* trace, const as_models_t* models,
  *   beta            latency slope, finite, >= 0 (1: a batch of b takes b times
  *                   as long as one request, as for GPUs a small batch saturates)
  *   max_batch       >= 1
- *   queue_cap       capacity of each model's queue per job, a power of two;
- *                   the queues live in LDS (M * queue_cap * 4 bytes per job,
- *                   AS_E_LIMITS if that and the tables exceed a workgroup's LDS);
- *                   if a queue would overflow, the call returns AS_E_LIMITS
- *                   and its results are incomplete
+ *   queue_cap       the longest queue a model may reach in a job, a power of
+ *                   two in 1..2^20; if a queue would grow past it the call
+ *                   returns AS_E_LIMITS and its results are incomplete (the
+ *                   queues take no memory of their own: a queue is always a
+ *                   run of its model's arrivals, kept as two positions in a
+ *                   per-model arrival list the call builds once for all jobs).
+ *                   The stage-latency table must fit in a workgroup's LDS
+ *                   (M * pow2ceil(C) * Smax * 8 bytes), else AS_E_LIMITS
  *   out_served[J]   served counts
  *   out_digest[J][2] {h, fin_sum} or NULL, where h = sum mod 2^64 over served
  *                   requests i of mix(i), mix the SplitMix64 finaliser
@@ -328,8 +331,12 @@ int as_simulate_stats(const as_trace_t* trace, const as_models_t* models,
  *                   accept-word fold of the other entry points does not apply)
  *   finish_jobs, n_finish, out_finish as for as_simulate_placements (finish
  *                   time of a served request, -1 dropped, -2 no hosting group)
- * Synchronous on `stream` (it reads back the overflow flag); allocates 4
- * bytes of device memory per call.  One job per wavefront, lanes = groups.
+ * Synchronous on `stream` (it reads back a flags word); allocates about
+ * 24 bytes of device memory per request of the trace per call (the arrival
+ * lists) and frees it before returning.  AS_E_INVALID_DATA if a queue is ever
+ * found not to be such a run (the rules rule it out; the check guards the
+ * results).  One job per wavefront: lanes = groups for the free times,
+ * lanes = models for the queues.
  */
 int as_simulate_batched(const as_trace_t* trace, const as_models_t* models,
                         const as_placements_t* placements, const double* slo_scale, int32_t n_scales,

@@ -5,17 +5,29 @@
 // grows linearly with its size.  The exact rules are those of
 // alpaserve_sim.h's as_simulate_batched.
 //
-// Layout: one job per wavefront (one wavefront per workgroup), lane g = group
-// g: a group's stage free times live in its lane's registers.  The job's
-// per-model FIFO queues are ring buffers of trace indices in LDS, with their
-// head/tail counters beside them; which models have queued requests is a
-// wave-uniform 64-bit mask.  Every decision is wave-uniform: the next idle
-// group is a butterfly min over the lanes with queued work, the model with the
-// oldest queued head a scalar loop over the group's models, and the batch
-// size a loop over b in which every lane runs its own stage chain and the
-// chosen lane's finish is read back.  The arithmetic is the definition's
-// (no FMA, v_max_f64, the batch factor rounded once), so served counts,
-// digests and finish times are bit-identical to a sequential evaluation.
+// A queue needs no storage of its own.  A request joins its model's queue
+// only when no hosting group is available at its arrival, and a group that
+// is available then has already drained every queue of the models it hosts
+// (the idle events up to the arrival are handled first, and a group with
+// queued work stays busy or takes that work).  So an arrival served or
+// dropped at once finds its model's queue empty, and a non-empty queue holds
+// every arrival of its model since its head.  Requests leave a queue only at
+// its head.  A queue is therefore a run [head, tail) of its model's arrivals
+// in trace order: the launch first lists each model's arrivals (time, trace
+// index, digest term) once for all jobs, and a job keeps per model only two
+// positions in that list and its head's time and index.
+//
+// Layout: one job per wavefront (one wavefront per workgroup).  Lane g holds
+// group g's stage free times; lane m holds model m's queue (positions, head
+// time and index, SLO); the trace is read 64 requests at a time into
+// registers.  Every decision is wave-uniform: the next idle group is a
+// butterfly min over the lanes with queued work, the model with the oldest
+// queued head a scalar pass over lane reads, and the batch size one pass in
+// which lane l runs the chain of a batch of l + 1 requests.  Only the
+// stage-latency table sits in LDS, so every job of a launch is resident at
+// once.  The arithmetic is the definition's (no FMA, v_max_f64, the batch
+// factor rounded once), so served counts, digests and finish times are
+// bit-identical to a sequential evaluation.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -27,6 +39,25 @@
 
 namespace as_dev {
 namespace {
+
+// Per-model arrival lists of a trace: the requests of model m in trace order
+// occupy positions [off[m], off[m + 1]) of lt (arrival time), li (trace
+// index) and lmix (the digest term of the index); ord[i] is request i's rank
+// among its model's requests (0 for requests of no model).
+struct ListArgs {
+  const double* t;
+  const int32_t* model;
+  int64_t n;
+  int32_t M;
+  uint32_t* blk;  // [nblk][M] requests of each model per block, then the exclusive prefix over blocks
+  int64_t nblk;
+  uint32_t* off;  // [M + 1]
+  uint32_t* ord;  // [n]
+  double* lt;     // [n]
+  uint32_t* li;   // [n]
+  uint64_t* lmix; // [n]
+  uint32_t* flags;  // the batch kernel's flags word (cleared here)
+};
 
 struct BatchArgs {
   const double* t;
@@ -40,7 +71,12 @@ struct BatchArgs {
   int64_t* out_served;
   uint64_t* out_digest;
   double* out_finish;
-  uint32_t* overflow;  // set when a queue would exceed its capacity
+  uint32_t* flags;  // bit 0: a queue would exceed its capacity; bit 1: a queue broke the run invariant
+  const uint32_t* off;
+  const uint32_t* ord;
+  const double* lt;
+  const uint32_t* li;
+  const uint64_t* lmix;
   double beta;
   int32_t M, C, smax_in, G, K, J, max_batch, qcap, n_finish;
   int32_t cfg_stages[AS_MAX_CONFIGS];
@@ -60,13 +96,97 @@ __device__ __forceinline__ double rl_f64(double v, int lane) {
   return __hiloint2double(hi, lo);
 }
 
-constexpr int kBatchChunk = 512;  // trace requests staged per LDS refill
+__device__ __forceinline__ uint64_t rl_u64(uint64_t v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
 
-// LDS of one job: queue entries (trace index and deadline) [M][qcap], heads
-// and tails [M], SLOs [M], stage-latency table [M][Cp][SMAX], trace chunk.
-__host__ __device__ constexpr size_t batch_lds_bytes(int M, int Cp, int SMAX, int qcap) {
-  return (size_t)M * qcap * 12 + (size_t)M * 8 + (size_t)M * 8 + (size_t)M * Cp * SMAX * 8 +
-         (size_t)kBatchChunk * 12;
+constexpr int kListBlock = 4096;  // trace requests per wavefront of the list kernels
+
+// Walks one block's requests 64 at a time; for every chunk, body(i, ok, x,
+// rank_base, mask) is called once per distinct model x of the chunk, where
+// mask holds the chunk's lanes with model x and rank_base the number of
+// earlier requests of x in the block (held in lane x of cnt).
+template <class Body>
+__device__ __forceinline__ void list_walk(const ListArgs& a, int64_t blk, uint32_t& cnt, Body body) {
+  const int lane = threadIdx.x;
+  const uint64_t below = (1ull << lane) - 1;
+  const int64_t b = blk * kListBlock, e = std::min<int64_t>(a.n, b + kListBlock);
+  for (int64_t c = b; c < e; c += 64) {
+    const int64_t i = c + lane;
+    const int x = i < e ? a.model[i] : -1;
+    const bool ok = (unsigned)x < (unsigned)a.M;
+    uint64_t rem = __builtin_amdgcn_ballot_w64(ok);
+    uint32_t rank = 0;
+    while (rem) {
+      const int xm = __builtin_amdgcn_readlane(x, __builtin_ctzll(rem));
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(ok && x == xm);
+      const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)cnt, xm);
+      if (ok && x == xm) rank = base + (uint32_t)__builtin_popcountll(mask & below);
+      if (lane == xm) cnt += (uint32_t)__builtin_popcountll(mask);
+      rem &= ~mask;
+    }
+    body(i, i < e, ok, x, rank);
+  }
+}
+
+// Requests of each model per block.
+__global__ __launch_bounds__(64) void list_count(const ListArgs a) {
+  uint32_t cnt = 0;
+  list_walk(a, blockIdx.x, cnt, [](int64_t, bool, bool, int, uint32_t) {});
+  if ((int)threadIdx.x < a.M) a.blk[(int64_t)blockIdx.x * a.M + threadIdx.x] = cnt;
+}
+
+// Exclusive prefixes: per model over the blocks, then over the models.
+__global__ __launch_bounds__(64) void list_scan(const ListArgs a) {
+  const int lane = threadIdx.x;
+  uint32_t run = 0;
+  if (lane < a.M) {
+    for (int64_t b = 0; b < a.nblk; b += 8) {  // 8 loads in flight at a time
+      uint32_t v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = b + k < a.nblk ? a.blk[(b + k) * a.M + lane] : 0u;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (b + k < a.nblk) a.blk[(b + k) * a.M + lane] = run;
+        run += v[k];
+      }
+    }
+  }
+  uint32_t acc = 0, mine = 0;
+  for (int m = 0; m < a.M; ++m) {
+    if (lane == m) mine = acc;
+    acc += (uint32_t)__builtin_amdgcn_readlane((int)run, m);
+  }
+  if (lane < a.M) a.off[lane] = mine;
+  if (lane == 0) {
+    a.off[a.M] = acc;
+    *a.flags = 0u;
+  }
+}
+
+// Ranks and list entries.
+__global__ __launch_bounds__(64) void list_fill(const ListArgs a) {
+  const int lane = threadIdx.x;
+  uint32_t cnt = lane < a.M ? a.blk[(int64_t)blockIdx.x * a.M + lane] : 0;
+  const uint32_t offl = lane < a.M ? a.off[lane] : 0;
+  list_walk(a, blockIdx.x, cnt, [&](int64_t i, bool in, bool ok, int x, uint32_t rank) {
+    const uint32_t o = (uint32_t)__builtin_amdgcn_ds_bpermute((ok ? x : 0) << 2, (int)offl);
+    if (!in) return;
+    a.ord[i] = ok ? rank : 0u;
+    if (ok) {
+      const uint32_t pos = o + rank;
+      a.lt[pos] = a.t[i];
+      a.li[pos] = (uint32_t)i;
+      a.lmix[pos] = mix64((uint64_t)i);
+    }
+  });
+}
+
+// LDS of one job: the stage-latency table [M][Cp][SMAX].
+__host__ __device__ constexpr size_t batch_lds_bytes(int M, int Cp, int SMAX) {
+  return (size_t)M * Cp * SMAX * 8;
 }
 
 // W: lanes reduced per job, the group count rounded up to a power of two (at
@@ -76,19 +196,11 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   int cp = 1;
   while (cp < a.C) cp <<= 1;
-  double* sL = reinterpret_cast<double*>(smem);                   // [M][cp][SMAX]
-  double* sSlo = sL + (size_t)a.M * cp * SMAX;                    // [M]
-  double* sQd = sSlo + a.M;                                       // [M][qcap] deadlines
-  double* sT = sQd + (size_t)a.M * a.qcap;                        // chunk times
-  uint32_t* sHead = reinterpret_cast<uint32_t*>(sT + kBatchChunk);  // [M]
-  uint32_t* sTail = sHead + a.M;                                  // [M]
-  uint32_t* sQi = sTail + a.M;                                    // [M][qcap] trace indices
-  int32_t* sM = reinterpret_cast<int32_t*>(sQi + (size_t)a.M * a.qcap);  // chunk models
+  double* sL = reinterpret_cast<double*>(smem);  // [M][cp][SMAX]
   const int lane = threadIdx.x;
   const int64_t job = blockIdx.x;
   const int p = (int)(job / a.K);
   const double sigma = a.slo_scale[job % a.K];
-  const uint32_t qmask = (uint32_t)a.qcap - 1u;
 
   int cfg = lane < a.G ? a.group_cfg[(int64_t)p * a.G + lane] : -1;
   if (cfg >= a.C || cfg < 0) cfg = -1;
@@ -105,30 +217,35 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
     const int m = mc / cp;
     sL[idx] = (c < a.C && s < a.cfg_stages[c]) ? a.stage_lat[((int64_t)m * a.C + c) * a.smax_in + s] : 0.0;
   }
-  for (int m = lane; m < a.M; m += 64) {
-    sSlo[m] = sigma * a.d_single[m];
-    sHead[m] = 0;
-    sTail[m] = 0;
-  }
   int frow = -1;
   for (int f = 0; f < a.n_finish; ++f)
     if (a.finish_jobs[f] == job) frow = f;
   double* frowp = frow >= 0 ? a.out_finish + (int64_t)frow * a.n : nullptr;
   __syncthreads();
 
+  // lane m: model m's SLO and queue, the run [qh, qt) of its list starting
+  // at loff, with the head's arrival time and trace index
+  const bool mlane = lane < a.M;
+  const double slo = mlane ? sigma * a.d_single[lane] : 0.0;
+  const uint32_t loff = mlane ? a.off[lane] : 0u;
+  uint32_t qh = 0, qt = 0, qidx = 0;
+  double qht = 0.0;
+  uint64_t nonempty = 0;  // bit m: model m has queued requests (wave-uniform)
+
   const double* lbase = sL + (size_t)(cfg < 0 ? 0 : cfg) * SMAX;  // + m * cp * SMAX
   double F[SMAX];
 #pragma unroll
   for (int s = 0; s < SMAX; ++s) F[s] = 0.0;
-  uint64_t nonempty = 0;  // bit m: model m has queued requests (wave-uniform)
-  uint64_t h = 0, fin_sum = 0;
+  uint64_t h = 0, fin_sum = 0;  // wave-uniform parts of the digest
+  uint64_t hl = 0, pend = 0;    // per-lane digest terms of batched requests (pend: the last batch's, in flight)
   int64_t served = 0;
+  uint32_t flags = 0;
   const double kInf = __builtin_inf();
 
-  // every lane's chain for a batch of b requests of model m started at x;
-  // returns the last stage's finish, fs[] its stage finishes
-  auto chain = [&](int m, int b, double x, double (&fs)[SMAX]) {
-    const double fac = 1.0 + a.beta * (double)(b - 1);
+  // every lane's chain, through its own group, for one request of model m
+  // started at x; returns the last stage's finish, fs[] its stage finishes
+  auto chain1 = [&](int m, double x, double (&fs)[SMAX]) {
+    const double fac = 1.0 + a.beta * 0.0;
     const double* L = lbase + (size_t)m * cp * SMAX;
     double f = x;
 #pragma unroll
@@ -143,21 +260,39 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
     const double v = seg_min<W>(key);
     return rl_f64(v, 0);
   };
-
-  for (int64_t base = 0; base <= a.n; base += kBatchChunk) {
-    const int cnt = (int)((a.n - base) < kBatchChunk ? (a.n - base) : kBatchChunk);
-    __syncthreads();
-    for (int e = lane; e < cnt; e += 64) {
-      sT[e] = a.t[base + e];
-      sM[e] = a.model[base + e];
+  // model mc's queue head moves to list position hn (< tail: its entry is
+  // loaded by lane mc; the value is first needed at the next decision)
+  auto set_head = [&](int mc, uint32_t hn, uint32_t tl) {
+    if (lane == mc) qh = hn;
+    if (hn == tl) {
+      nonempty &= ~(1ull << mc);
+    } else if (lane == mc) {
+      qht = a.lt[loff + hn];
+      qidx = a.li[loff + hn];
     }
-    __syncthreads();
+  };
+
+  // the trace, 64 requests per register chunk, the next chunk in flight
+  auto load_chunk = [&](int64_t base, double& tv, int& mv, uint32_t& ov) {
+    const int64_t i = base + lane;
+    tv = i < a.n ? a.t[i] : 0.0;
+    mv = i < a.n ? a.model[i] : -1;
+    ov = i < a.n ? a.ord[i] : 0u;
+  };
+  double tv, tvn = 0.0;
+  int mv, mvn = -1;
+  uint32_t ov, ovn = 0;
+  load_chunk(0, tv, mv, ov);
+
+  for (int64_t base = 0; base <= a.n; base += 64) {
+    const int cnt = (int)((a.n - base) < 64 ? (a.n - base) : 64);
+    if (base + 64 < a.n) load_chunk(base + 64, tvn, mvn, ovn);
     // cnt requests of this chunk, then (after the last one) the final drain
-    const int steps = base + kBatchChunk > a.n ? cnt + 1 : cnt;
+    const int steps = base + 64 > a.n ? cnt + 1 : cnt;
     for (int e = 0; e < steps; ++e) {
       const bool last = e == cnt;
       const int64_t i = base + e;
-      const double horizon = last ? 0.0 : sT[e];
+      const double horizon = last ? 0.0 : rl_f64(tv, e);
       // idle events up to the arrival (all remaining ones after the last)
       for (;;) {
         const bool work = cfg >= 0 && (hostbits & nonempty) != 0;
@@ -167,68 +302,93 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
         if (wm == 0) break;
         if (!last && !(mn <= horizon)) break;
         const int g = __builtin_ctzll(wm);
-        const uint64_t ghost = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(hostbits >> 32), g) << 32) |
-                               (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)hostbits, g);
+        const uint64_t ghost = rl_u64(hostbits, g);
+        const int gcfg = __builtin_amdgcn_readlane(cfg, g);
+        double Fg[SMAX];
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s) Fg[s] = rl_f64(F[s], g);
         for (;;) {
           uint64_t cand = ghost & nonempty;
           if (cand == 0) break;  // nothing left for this group: it stays idle
-          int mc = -1;
-          uint32_t hidx = 0;
+          // the queued model whose head has the lowest trace index
+          int mc = __builtin_ctzll(cand);
+          uint32_t hidx = (uint32_t)__builtin_amdgcn_readlane((int)qidx, mc);
+          cand &= cand - 1;
           while (cand) {
             const int m = __builtin_ctzll(cand);
             cand &= cand - 1;
-            const uint32_t r = sQi[(size_t)m * a.qcap + (sHead[m] & qmask)];
-            if (mc < 0 || r < hidx) {
+            const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)qidx, m);
+            if (r < hidx) {
               mc = m;
               hidx = r;
             }
           }
-          const uint32_t h0 = sHead[mc];
-          const double dl = sQd[(size_t)mc * a.qcap + (h0 & qmask)];
-          const uint32_t avail = sTail[mc] - h0;
+          const uint32_t h0 = (uint32_t)__builtin_amdgcn_readlane((int)qh, mc);
+          const uint32_t tl = (uint32_t)__builtin_amdgcn_readlane((int)qt, mc);
+          const double dl = rl_f64(qht + slo, mc);  // the head's deadline
+          const uint32_t avail = tl - h0;
           const int bmax = (int)(avail < (uint32_t)a.max_batch ? avail : (uint32_t)a.max_batch);
+          // the largest batch meeting the deadline: the sizes are tried 64 at
+          // a time, lane l the size p0 + l + 1, and the first size that
+          // misses ends the search (as trying them one by one would)
+          const double* L = sL + ((size_t)mc * cp + gcfg) * SMAX;
           int b = 0;
           double fin = 0.0;
-          double fs[SMAX];
-          for (int bb = 1; bb <= bmax; ++bb) {
-            double fsb[SMAX];
-            const double fl = rl_f64(chain(mc, bb, mn, fsb), g);
-            if (fl > dl) break;
-            b = bb;
-            fin = fl;
+          double fsel[SMAX];
 #pragma unroll
-            for (int s = 0; s < SMAX; ++s) fs[s] = fsb[s];
+          for (int s = 0; s < SMAX; ++s) fsel[s] = 0.0;
+          for (int p0 = 0; p0 < bmax; p0 += 64) {
+            const int bb = p0 + lane + 1;
+            const double fac = 1.0 + a.beta * (double)(bb - 1);
+            double f = mn;
+            double fs[SMAX];
+#pragma unroll
+            for (int s = 0; s < SMAX; ++s) {
+              fs[s] = vmax(f, Fg[s]) + L[s] * fac;
+              f = fs[s];
+            }
+            const uint64_t miss = __builtin_amdgcn_ballot_w64(bb <= bmax && f > dl);
+            const int lim = bmax - p0 < 64 ? bmax - p0 : 64;
+            const int nok = miss ? __builtin_ctzll(miss) : lim;  // sizes p0+1 .. p0+nok meet it
+            if (nok > 0) {
+              b = p0 + nok;
+              fin = rl_f64(f, nok - 1);
+#pragma unroll
+              for (int s = 0; s < SMAX; ++s) fsel[s] = rl_f64(fs[s], nok - 1);
+            }
+            if (nok < 64) break;
           }
           if (b == 0) {
             // the head cannot meet its deadline: dropped (its output stays -1)
-            __syncthreads();
-            if (lane == 0) sHead[mc] = h0 + 1;
-            __syncthreads();
-            if (h0 + 1 == sTail[mc]) nonempty &= ~(1ull << mc);
+            set_head(mc, h0 + 1, tl);
             continue;
           }
           if (lane == g) {
 #pragma unroll
-            for (int s = 0; s < SMAX; ++s) F[s] = fs[s];
+            for (int s = 0; s < SMAX; ++s) F[s] = fsel[s];
           }
-          for (int k = 0; k < b; ++k) {
-            const uint32_t r = sQi[(size_t)mc * a.qcap + ((h0 + k) & qmask)];
-            h += mix64(r);
-            fin_sum += (uint64_t)__double_as_longlong(fin);
-            if (frowp && lane == 0) frowp[r] = fin;
-          }
+          // the batch's digest terms: the first 64 arrive while the
+          // simulation goes on and are added at the next batch
+          const uint32_t lb0 = (uint32_t)__builtin_amdgcn_readlane((int)loff, mc) + h0;
+          hl += pend;
+          pend = 0;
+          if (lane < b) pend = a.lmix[lb0 + lane];
+          for (int k0 = 64; k0 < b; k0 += 64)
+            if (k0 + lane < b) hl += a.lmix[lb0 + k0 + lane];
+          fin_sum += (uint64_t)b * (uint64_t)__double_as_longlong(fin);
           served += b;
-          __syncthreads();
-          if (lane == 0) sHead[mc] = h0 + b;
-          __syncthreads();
-          if (h0 + b == sTail[mc]) nonempty &= ~(1ull << mc);
+          if (frowp) {
+            for (int k0 = 0; k0 < b; k0 += 64)
+              if (k0 + lane < b) frowp[a.li[lb0 + k0 + lane]] = fin;
+          }
+          set_head(mc, h0 + (uint32_t)b, tl);
           break;
         }
       }
       if (last) break;
       // the arrival
       const double ti = horizon;
-      const int m0 = sM[e];
+      const int m0 = __builtin_amdgcn_readlane(mv, e);
       const bool mok = (unsigned)m0 < (unsigned)a.M;
       const int m = mok ? m0 : 0;
       const bool hosted = mok && cfg >= 0 && ((hostbits >> m) & 1u);
@@ -240,8 +400,8 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
         const double mn = wave_min(key);
         const int ga = __builtin_ctzll(__builtin_amdgcn_ballot_w64(avail && key == mn));
         double fs[SMAX];
-        const double fl = rl_f64(chain(m, 1, ti, fs), ga);
-        if (!(fl > ti + sSlo[m])) {
+        const double fl = rl_f64(chain1(m, ti, fs), ga);
+        if (!(fl > ti + rl_f64(slo, m))) {
           if (lane == ga) {
 #pragma unroll
             for (int s = 0; s < SMAX; ++s) F[s] = fs[s];
@@ -268,29 +428,39 @@ __global__ __launch_bounds__(64) void batch_kernel(const BatchArgs a) {
           for (int s = 0; s < SMAX; ++s) lbv = lbv + L[s];
         }
         const double lb = wave_min(hosted ? lbv : kInf);
-        uint32_t hd = sHead[m];
-        const uint32_t tl = sTail[m];
-        while (hd != tl && sQd[(size_t)m * a.qcap + (hd & qmask)] < lb) ++hd;
-        if (tl - hd == (uint32_t)a.qcap) {
-          if (lane == 0) atomicOr(a.overflow, 1u);  // queue full: the request is lost
-        } else {
-          __syncthreads();
-          if (lane == 0) {
-            sHead[m] = hd;
-            sQi[(size_t)m * a.qcap + (tl & qmask)] = (uint32_t)i;
-            sQd[(size_t)m * a.qcap + (tl & qmask)] = ti + sSlo[m];
-            sTail[m] = tl + 1;
-          }
-          __syncthreads();
-          nonempty |= 1ull << m;
+        const uint32_t rank = (uint32_t)__builtin_amdgcn_readlane((int)ov, e);
+        uint32_t hd = (uint32_t)__builtin_amdgcn_readlane((int)qh, m);
+        const uint32_t tl = (uint32_t)__builtin_amdgcn_readlane((int)qt, m);
+        while (hd != tl && rl_f64(qht + slo, m) < lb) {
+          ++hd;
+          set_head(m, hd, tl);
         }
+        if (hd == tl) {
+          // an empty queue: request i becomes its head
+          if (lane == m) {
+            qh = rank;
+            qht = ti;
+            qidx = (uint32_t)i;
+          }
+        } else {
+          if (rank != tl) flags |= 2u;  // not the run's next arrival (cannot happen by the rules)
+          if (tl - hd >= (uint32_t)a.qcap) flags |= 1u;  // past the capacity: the results are incomplete
+        }
+        if (lane == m) qt = rank + 1;
+        nonempty |= 1ull << m;
       }
     }
+    tv = tvn;
+    mv = mvn;
+    ov = ovn;
   }
+  hl += pend;
+  const uint64_t hsum = seg_sum_u64<64>(hl);
   if (lane == 0) {
+    if (flags) atomicOr(a.flags, flags);
     a.out_served[job] = served;
     if (a.out_digest) {
-      a.out_digest[2 * job] = h;
+      a.out_digest[2 * job] = h + hsum;
       a.out_digest[2 * job + 1] = fin_sum;
     }
   }
@@ -355,9 +525,9 @@ extern "C" int as_simulate_batched(const as_trace_t* trace, const as_models_t* m
       if (finish_jobs[q] == finish_jobs[f]) return fail(AS_E_INVALID_ARG, "finish_jobs[%d] repeats job %d", f, finish_jobs[f]);
     a.finish_jobs[f] = finish_jobs[f];
   }
-  const size_t lds = as_dev::batch_lds_bytes(ka.M, pow2ceil(ka.C), smax, queue_cap);
+  const size_t lds = as_dev::batch_lds_bytes(ka.M, pow2ceil(ka.C), smax);
   if (lds > shared_lds_limit())
-    return fail(AS_E_LIMITS, "batched: queues and tables need %zu bytes of LDS (> %zu); lower queue_cap", lds,
+    return fail(AS_E_LIMITS, "batched: the stage-latency table needs %zu bytes of LDS (> %zu)", lds,
                 shared_lds_limit());
   if (J == 0) return ok();
   hipStream_t s = (hipStream_t)stream;
@@ -383,11 +553,38 @@ extern "C" int as_simulate_batched(const as_trace_t* trace, const as_models_t* m
   a.qcap = queue_cap;
   a.n_finish = n_finish;
   for (int c = 0; c < AS_MAX_CONFIGS; ++c) a.cfg_stages[c] = ka.cfg_stages[c];
-  uint32_t* d_flag = nullptr;
-  hipError_t e = hipMallocAsync((void**)&d_flag, sizeof(uint32_t), s);
-  if (e != hipSuccess) return fail(AS_E_NOMEM, "hipMallocAsync: %s", hipGetErrorString(e));
-  a.overflow = d_flag;
-  e = hipMemsetAsync(d_flag, 0, sizeof(uint32_t), s);
+  // one workspace: the flags word, then the per-model arrival lists
+  as_dev::ListArgs la;
+  std::memset(&la, 0, sizeof la);
+  la.t = trace->t;
+  la.model = trace->model;
+  la.n = trace->n;
+  la.M = ka.M;
+  la.nblk = (trace->n + as_dev::kListBlock - 1) / as_dev::kListBlock;
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t n = (size_t)trace->n;
+  const size_t o_blk = 256, o_off = o_blk + up((size_t)la.nblk * ka.M * 4), o_ord = o_off + up((size_t)(ka.M + 1) * 4),
+               o_lt = o_ord + up(n * 4), o_li = o_lt + up(n * 8), o_mix = o_li + up(n * 4), total = o_mix + up(n * 8);
+  unsigned char* ws = nullptr;
+  hipError_t e = hipMallocAsync((void**)&ws, total, s);
+  if (e != hipSuccess) return fail(AS_E_NOMEM, "hipMallocAsync(%zu): %s", total, hipGetErrorString(e));
+  a.flags = reinterpret_cast<uint32_t*>(ws);
+  la.flags = a.flags;
+  la.blk = reinterpret_cast<uint32_t*>(ws + o_blk);
+  la.off = reinterpret_cast<uint32_t*>(ws + o_off);
+  la.ord = reinterpret_cast<uint32_t*>(ws + o_ord);
+  la.lt = reinterpret_cast<double*>(ws + o_lt);
+  la.li = reinterpret_cast<uint32_t*>(ws + o_li);
+  la.lmix = reinterpret_cast<uint64_t*>(ws + o_mix);
+  a.off = la.off;
+  a.ord = la.ord;
+  a.lt = la.lt;
+  a.li = la.li;
+  a.lmix = la.lmix;
+  if (la.nblk > 0) hipLaunchKernelGGL(as_dev::list_count, dim3((unsigned)la.nblk), dim3(64), 0, s, la);
+  hipLaunchKernelGGL(as_dev::list_scan, dim3(1), dim3(64), 0, s, la);  // also clears the flags
+  if (la.nblk > 0) hipLaunchKernelGGL(as_dev::list_fill, dim3((unsigned)la.nblk), dim3(64), 0, s, la);
+  e = hipGetLastError();
   if (e == hipSuccess && n_finish > 0 && a.n > 0) {
     const int64_t cells = (int64_t)n_finish * a.n;
     const int blocks = (int)std::min<int64_t>((cells + 255) / 256, 8192);
@@ -415,11 +612,13 @@ extern "C" int as_simulate_batched(const as_trace_t* trace, const as_models_t* m
     e = hipGetLastError();
   }
   uint32_t flag = 0;
-  if (e == hipSuccess) e = hipMemcpyAsync(&flag, d_flag, sizeof flag, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(&flag, a.flags, sizeof flag, hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
-  const hipError_t ef = hipFreeAsync(d_flag, s);
+  const hipError_t ef = hipFreeAsync(ws, s);
   if (e == hipSuccess) e = ef;
   if (e != hipSuccess) return fail(AS_E_HIP, "batched: %s", hipGetErrorString(e));
-  if (flag) return fail(AS_E_LIMITS, "batched: a model queue exceeded queue_cap=%d; results are incomplete", queue_cap);
+  if (flag & 2u)
+    return fail(AS_E_INVALID_DATA, "batched: a queue was not a run of its model's arrivals; results are invalid");
+  if (flag & 1u) return fail(AS_E_LIMITS, "batched: a model queue exceeded queue_cap=%d; results are incomplete", queue_cap);
   return ok();
 }
