@@ -24,6 +24,7 @@ SIM_API_SRC = os.path.join(CSRC, "sim_api.hip")
 SIM_LAUNCH_SRC = os.path.join(CSRC, "sim_launch.hip")
 SIM_SEARCH_SRC = os.path.join(CSRC, "sim_search.hip")
 SIM_STATS_SRC = os.path.join(CSRC, "sim_stats.hip")
+SIM_MULTI_SRC = os.path.join(CSRC, "sim_multi.hip")
 SIM_ALG2_SRC = os.path.join(CSRC, "sim_alg2.hip")
 SIM_BATCH_SRC = os.path.join(CSRC, "sim_batch.hip")
 SIM_SPEC_SRC = os.path.join(CSRC, "sim_spec.hip")
@@ -72,7 +73,8 @@ def build_sim(extra_flags=(), jobs=None) -> str:
              (SIM_STATS_SRC, os.path.join(obj_dir, "sim_stats.o"), []),
              (SIM_ALG2_SRC, os.path.join(obj_dir, "sim_alg2.o"), []),
              (SIM_BATCH_SRC, os.path.join(obj_dir, "sim_batch.o"), []),
-             (SIM_SPEC_SRC, os.path.join(obj_dir, "sim_spec.o"), [])]
+             (SIM_SPEC_SRC, os.path.join(obj_dir, "sim_spec.o"), []),
+             (SIM_MULTI_SRC, os.path.join(obj_dir, "sim_multi.o"), [])]
     for w in LANE_WIDTHS:
         units.append((SIM_LAUNCH_SRC, os.path.join(obj_dir, f"sim_launch_w{w}.o"), [f"-DAS_W={w}"]))
 

@@ -341,6 +341,53 @@ int run_shared_stats(KArgs& a, int smax, hipStream_t stream) {
   return ok();
 }
 
+// Multi-shape dispatches pay where the jobs are few: a step whose shapes run
+// on separate streams costs a trace pass of latency per shape that shares a
+// hardware queue.  Where the blocks fill the device many times over, launches
+// of their own shapes run faster (the multi-shape kernel holds the registers
+// and LDS of its largest shape), and they overlap anyway.
+constexpr int64_t kMultiMaxBlocks = 2048;
+
+int run_shared_multi(const KArgs& a, void* dev_args, const ShapeJobs* sh, int n, bool stats, hipStream_t stream) {
+  if (!use_shared_path() || a.K != 1 || a.n_finish != 0 || n < 1 || n > as_dev::kMaxShapeSegs || !dev_args)
+    return AS_E_LIMITS;
+  size_t lds = 0;
+  as_dev::MultiSegs ms;
+  std::memset(&ms, 0, sizeof ms);
+  int64_t blocks = 0;
+  for (int i = 0; i < n; ++i) {
+    const int W = sh[i].W, sm = sh[i].smax;
+    if (W < 1 || W > 64 || (W & (W - 1)) != 0 || sh[i].v.G > W || (sm != 1 && sm != 2 && sm != 4 && sm != 8))
+      return AS_E_LIMITS;
+    if (sh[i].v.J <= 0) continue;
+    if (!stats) {
+      KArgs ak = a;
+      ak.J = sh[i].v.J;
+      ak.G = sh[i].v.G;
+      if (want_spec(ak, sm) && spec_takes(ak, sm)) return AS_E_LIMITS;
+    }
+    const size_t l = as_dev::shared_lds_bytes(a.M, pow2ceil(a.C), sm) +
+                     (stats ? as_dev::shared_stats_lds_bytes(W, a.M) : 0);
+    lds = std::max(lds, l);
+    as_dev::ShapeSeg& g = ms.s[ms.n++];
+    int wl = 0, sl = 0;
+    while ((1 << wl) < W) ++wl;
+    while ((1 << sl) < sm) ++sl;
+    g.wl = wl;
+    g.sl = sl;
+    g.block0 = blocks;
+    g.v = sh[i].v;
+    const int64_t slots = (int64_t)(64 / W) * as_dev::kWaves;
+    blocks += (sh[i].v.J + slots - 1) / slots;
+  }
+  if (lds > shared_lds_limit() || blocks > kMultiMaxBlocks) return AS_E_LIMITS;
+  if (ms.n == 0) return ok();
+  hipError_t e = hipMemcpyAsync(dev_args, &a, sizeof(KArgs), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = launch_shared_multi(stats, static_cast<const KArgs*>(dev_args), ms, blocks, lds, stream);
+  if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 // The shared-trace kernel (one group per lane, W = G rounded up to a power of
 // two) unless its tables exceed the LDS of a workgroup; then the general
 // kernel, whose tables are smaller.  With only_check, whether one of them

@@ -7,6 +7,7 @@
 
 #include "alpaserve_sim.h"
 #include "sim_kernel.hpp"
+#include "sim_shared.hpp"
 
 namespace as_host {
 
@@ -54,6 +55,26 @@ int run_spec(KArgs& a, int smax, hipStream_t stream, bool can_give_up, void* cal
 constexpr int kSpecScratchTooSmall = -100;
 // Whether a shared-trace call takes the segment-speculative kernels.
 bool want_spec(const KArgs& a, int smax);
+// Whether they would take it once wanted (sizes, LDS, segments that pay);
+// nothing is launched.
+bool spec_takes(const KArgs& a, int smax);
+
+// One shape of a multi-shape shared-trace launch: lanes per job W (a power
+// of two >= the group stride v.G), padded stages smax, and its jobs.
+struct ShapeJobs {
+  int W, smax;
+  as_dev::JobSet v;
+};
+// The jobs of up to 16 shapes (one SLO scale, no per-request rows) in one
+// dispatch, every job exactly as a launch of its own shape would simulate it
+// (stats: the statistics outputs too).  Returns AS_E_LIMITS without
+// launching when the jobs are too many for a multi-shape dispatch to pay
+// (more than 2048 workgroups) or some shape would not take the shared-trace
+// kernel as a launch of its own (the speculative kernels, LDS, the path
+// switched off); the caller then launches the shapes one by one.
+// dev_args: device memory of sizeof(KArgs) bytes for the common arguments,
+// not used by other work until these launches have run.
+int run_shared_multi(const KArgs& a, void* dev_args, const ShapeJobs* sh, int n, bool stats, hipStream_t stream);
 // Whether ALPASERVE_PATH=spec forces them (even with a single segment).
 bool spec_forced();
 

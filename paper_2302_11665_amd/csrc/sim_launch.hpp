@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include "sim_kernel.hpp"
+#include "sim_shared.hpp"
 
 namespace as_host {
 
@@ -18,6 +19,12 @@ hipError_t launch_lds(int gpl, int smax, bool seg, const KArgs& a, size_t lds, h
 // stats (one scale only): per-model served counts and per-group busy time.
 template <int W>
 hipError_t launch_shared(int smax, bool usig, bool stats, const KArgs& a, size_t lds, hipStream_t s);
+
+// Several shapes of the shared-trace kernel (one SLO scale, no per-request
+// rows) in one dispatch over `blocks` workgroups (sim_multi.hip); a_dev: the
+// common arguments in device memory, unchanged until the launch has run.
+hipError_t launch_shared_multi(bool stats, const KArgs* a_dev, const as_dev::MultiSegs& ms, int64_t blocks,
+                               size_t lds, hipStream_t s);
 
 // Segmented jobs with up to 64 groups, one job per wavefront (built in the
 // 64-lane unit).

@@ -63,8 +63,8 @@ struct StreamPool {
     return hipSuccess;
   }
   ~StreamPool() {
-    for (hipStream_t x : st) hipStreamDestroy(x);
-    for (hipEvent_t y : ev) hipEventDestroy(y);
+    for (hipStream_t x : st) (void)hipStreamDestroy(x);
+    for (hipEvent_t y : ev) (void)hipEventDestroy(y);
   }
 };
 
@@ -85,7 +85,7 @@ struct DevBufs {
   size_t cap[8] = {0};
   hipError_t need(int k, size_t bytes) {
     if (bytes <= cap[k]) return hipSuccess;
-    if (p[k]) hipFree(p[k]);
+    if (p[k]) (void)hipFree(p[k]);
     p[k] = nullptr;
     cap[k] = 0;
     const hipError_t e = hipMalloc(&p[k], bytes < 256 ? 256 : bytes);
@@ -94,7 +94,7 @@ struct DevBufs {
   }
   ~DevBufs() {
     for (void* q : p)
-      if (q) hipFree(q);
+      if (q) (void)hipFree(q);
   }
 };
 
@@ -295,11 +295,32 @@ int beam_search(const as_trace_t* trace, const as_models_t* models, const int64_
                          static_cast<int32_t*>(d.p[5]) + L.gofs);
       e = hipGetLastError();
     }
-    if (e == hipSuccess) e = pool.get(launches.size());
-    // the last event of the pool marks the expanded inputs on the caller's stream
-    if (e == hipSuccess) e = hipEventRecord(pool.ev[launches.size()], s);
+    if (e == hipSuccess) e = d.need(7, sizeof(KArgs));
     if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
-    for (size_t k = 0; k < launches.size(); ++k) {
+    // every shape in one dispatch; else one launch per shape, side by side
+    // on streams of their own
+    std::vector<ShapeJobs> shj;
+    for (const Launch& L : launches) {
+      ShapeJobs x;
+      x.W = shape_w[L.shape];
+      x.smax = shape_s[L.shape];
+      x.v = as_dev::JobSet{L.end - L.begin, shape_w[L.shape], static_cast<const int32_t*>(d.p[5]) + L.gofs,
+                           static_cast<const uint64_t*>(d.p[4]) + (size_t)L.begin * M,
+                           static_cast<int64_t*>(d.p[6]) + L.begin, nullptr, nullptr, nullptr, nullptr};
+      shj.push_back(x);
+    }
+    rc = run_shared_multi(a, d.p[7], shj.data(), (int)shj.size(), false, s);
+    if (rc != AS_E_LIMITS && rc != AS_OK) return rc;
+    const bool multi = rc == AS_OK;
+    if (multi && count) {
+      count->launches += 1;
+      count->jobs += P;
+    }
+    if (!multi && e == hipSuccess) e = pool.get(launches.size());
+    // the last event of the pool marks the expanded inputs on the caller's stream
+    if (!multi && e == hipSuccess) e = hipEventRecord(pool.ev[launches.size()], s);
+    if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+    for (size_t k = 0; !multi && k < launches.size(); ++k) {
       const Launch& L = launches[k];
       hipStream_t sk = launches.size() == 1 ? s : pool.st[k];
       if (sk != s && (e = hipStreamWaitEvent(sk, pool.ev[launches.size()], 0)) != hipSuccess)
@@ -373,18 +394,35 @@ int fast_search(const as_trace_t* trace, const as_models_t* models, const int64_
     cur[r] = Sel{std::vector<uint64_t>(M, 0), std::vector<int64_t>(probs[r].G, 0)};
     res[r].best_mask.assign(M, 0);
   }
-  std::vector<int32_t> cfg_tab((size_t)R * G, -1);
-  for (int r = 0; r < R; ++r)
-    for (int g = 0; g < probs[r].G; ++g) cfg_tab[(size_t)r * G + g] = probs[r].cfg[g];
+  // kernel shape of each problem: lanes per job (its group count rounded up
+  // to a power of two) and padded stage count (its deepest configuration);
+  // each step runs one statistics launch per shape, side by side, so a job's
+  // per-request chain is only as wide and as deep as its own partition
+  std::vector<int> shape_of(R), shape_w, shape_s;
+  for (int r = 0; r < R; ++r) {
+    int sm = 1;
+    for (int g = 0; g < probs[r].G; ++g)
+      if (probs[r].cfg[g] >= 0) sm = std::max(sm, models->cfg_stages[probs[r].cfg[g]]);
+    const int wr = pow2ceil(probs[r].G), sr = pow2ceil(sm);
+    int k = 0;
+    while (k < (int)shape_w.size() && !(shape_w[k] == wr && shape_s[k] == sr)) ++k;
+    if (k == (int)shape_w.size()) {
+      shape_w.push_back(wr);
+      shape_s.push_back(sr);
+    }
+    shape_of[r] = k;
+  }
+  const int Gp = pow2ceil(G);  // the widest row stride of a shape
+  StreamPool pool;
 
   DevBufs d;
-  hipError_t e = d.need(0, (size_t)R * G * 4);      // group configurations of the jobs
+  hipError_t e = d.need(0, (size_t)R * Gp * 4);     // group configurations of the jobs
   if (e == hipSuccess) e = d.need(1, 8);            // the scale
   if (e == hipSuccess) e = d.need(2, (size_t)M * 8);  // per-model request counts
   if (e == hipSuccess) e = d.need(3, (size_t)R * M * 8);  // masks
   if (e == hipSuccess) e = d.need(4, (size_t)R * 8);      // served
   if (e == hipSuccess) e = d.need(5, (size_t)R * M * 8);  // per-model served
-  if (e == hipSuccess) e = d.need(6, (size_t)R * G * 8);  // busy
+  if (e == hipSuccess) e = d.need(6, (size_t)R * Gp * 8);  // busy
   if (e != hipSuccess) return fail(AS_E_NOMEM, "search: device allocation failed: %s", hipGetErrorString(e));
   std::vector<unsigned long long> n_req(M, 0);
   e = hipMemcpyAsync(d.p[1], &slo_scale, 8, hipMemcpyHostToDevice, s);
@@ -404,37 +442,120 @@ int fast_search(const as_trace_t* trace, const as_models_t* models, const int64_
   std::vector<uint64_t> masks;
   std::vector<int64_t> served, ms;
   std::vector<double> busy;
+  struct Launch {
+    int shape, begin, end;
+    size_t gofs;  // first row entry of the shape's configuration and busy rows
+  };
+  std::vector<Launch> launches;
+  std::vector<size_t> brow;  // live job q: its busy row's first entry
   for (int step = 0;; ++step) {
     live.clear();
     for (int r = 0; r < R; ++r)
       if (active[r]) live.push_back(r);
     if (live.empty()) break;
+    std::stable_sort(live.begin(), live.end(), [&](int x, int y) { return shape_of[x] < shape_of[y]; });
     const int P = (int)live.size();
-    gcfg.assign((size_t)P * G, -1);
+    launches.clear();
+    brow.assign(P, 0);
+    size_t gtotal = 0;
+    for (int q = 0; q < P;) {
+      const int sh = shape_of[live[q]];
+      int q1 = q;
+      while (q1 < P && shape_of[live[q1]] == sh) ++q1;
+      launches.push_back({sh, q, q1, gtotal});
+      for (int x = q; x < q1; ++x) brow[x] = gtotal + (size_t)(x - q) * shape_w[sh];
+      gtotal += (size_t)(q1 - q) * shape_w[sh];
+      q = q1;
+    }
+    gcfg.assign(gtotal, -1);
     masks.clear();
     for (int q = 0; q < P; ++q) {
       const int r = live[q];
-      std::copy(cfg_tab.begin() + (size_t)r * G, cfg_tab.begin() + (size_t)(r + 1) * G, gcfg.begin() + (size_t)q * G);
+      std::copy(probs[r].cfg.begin(), probs[r].cfg.end(), gcfg.begin() + brow[q]);
       masks.insert(masks.end(), cur[r].mask.begin(), cur[r].mask.end());
     }
     e = hipMemcpyAsync(d.p[0], gcfg.data(), gcfg.size() * 4, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipMemcpyAsync(d.p[3], masks.data(), masks.size() * 8, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = d.need(7, sizeof(KArgs));
     if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
-    as_placements_t pl{P, G, static_cast<const int32_t*>(d.p[0]), static_cast<const uint64_t*>(d.p[3])};
-    rc = as_simulate_stats(trace, models, &pl, static_cast<const double*>(d.p[1]), 1,
-                           static_cast<int64_t*>(d.p[4]), nullptr, static_cast<int64_t*>(d.p[5]),
-                           static_cast<double*>(d.p[6]), s);
-    if (rc != AS_OK) return rc;
-    if (count) {
+    // every shape in one dispatch; else one launch per shape, side by side
+    // on streams of their own
+    KArgs am = a;
+    am.t = trace->t;
+    am.model = trace->model;
+    am.n = trace->n;
+    am.slo_scale = static_cast<const double*>(d.p[1]);
+    am.K = 1;
+    am.n_finish = 0;
+    std::vector<ShapeJobs> shj;
+    for (const Launch& L : launches)
+      shj.push_back(ShapeJobs{shape_w[L.shape], shape_s[L.shape],
+                              as_dev::JobSet{L.end - L.begin, shape_w[L.shape],
+                                             static_cast<const int32_t*>(d.p[0]) + L.gofs,
+                                             static_cast<const uint64_t*>(d.p[3]) + (size_t)L.begin * M,
+                                             static_cast<int64_t*>(d.p[4]) + L.begin, nullptr, nullptr,
+                                             static_cast<int64_t*>(d.p[5]) + (size_t)L.begin * M,
+                                             static_cast<double*>(d.p[6]) + L.gofs}});
+    rc = run_shared_multi(am, d.p[7], shj.data(), (int)shj.size(), true, s);
+    if (rc != AS_E_LIMITS && rc != AS_OK) return rc;
+    const bool multi = rc == AS_OK;
+    if (multi && count) {
       count->launches += 1;
       count->jobs += P;
     }
+    if (!multi && e == hipSuccess) e = pool.get(launches.size());
+    if (!multi && e == hipSuccess) e = hipEventRecord(pool.ev[launches.size()], s);
+    if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+    for (size_t k = 0; !multi && k < launches.size(); ++k) {
+      const Launch& L = launches[k];
+      hipStream_t sk = launches.size() == 1 ? s : pool.st[k];
+      if (sk != s && (e = hipStreamWaitEvent(sk, pool.ev[launches.size()], 0)) != hipSuccess)
+        return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+      const int Pk = L.end - L.begin, Gk = shape_w[L.shape];
+      const int32_t* gk = static_cast<const int32_t*>(d.p[0]) + L.gofs;
+      const uint64_t* mk = static_cast<const uint64_t*>(d.p[3]) + (size_t)L.begin * M;
+      int64_t* sv = static_cast<int64_t*>(d.p[4]) + L.begin;
+      int64_t* msv = static_cast<int64_t*>(d.p[5]) + (size_t)L.begin * M;
+      double* bz = static_cast<double*>(d.p[6]) + L.gofs;
+      KArgs ak = a;
+      ak.t = trace->t;
+      ak.model = trace->model;
+      ak.n = trace->n;
+      ak.slo_scale = static_cast<const double*>(d.p[1]);
+      ak.K = 1;
+      ak.P = Pk;
+      ak.J = Pk;
+      ak.G = Gk;
+      ak.group_cfg = gk;
+      ak.host_mask = mk;
+      ak.out_served = sv;
+      ak.out_digest = nullptr;
+      ak.out_model_served = msv;
+      ak.out_group_busy = bz;
+      ak.n_finish = 0;
+      rc = run_shared_stats(ak, shape_s[L.shape], sk);
+      if (rc == AS_E_LIMITS) {
+        // the shared-trace kernel does not take it: the general statistics kernel
+        as_placements_t pl{Pk, Gk, gk, mk};
+        rc = as_simulate_stats(trace, models, &pl, static_cast<const double*>(d.p[1]), 1, sv, nullptr, msv, bz,
+                               sk);
+      }
+      if (rc != AS_OK) return rc;
+      if (sk != s) {
+        if ((e = hipEventRecord(pool.ev[k], sk)) != hipSuccess || (e = hipStreamWaitEvent(s, pool.ev[k], 0)) != hipSuccess)
+          return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
+      }
+      if (count) {
+        count->launches += 1;
+        count->jobs += Pk;
+      }
+    }
     served.resize(P);
     ms.resize((size_t)P * M);
-    busy.resize((size_t)P * G);
+    busy.resize(gtotal);
     e = hipMemcpyAsync(served.data(), d.p[4], (size_t)P * 8, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(ms.data(), d.p[5], (size_t)P * M * 8, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(busy.data(), d.p[6], (size_t)P * G * 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(busy.data(), d.p[6], gtotal * 8, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(AS_E_HIP, "search: step %d: %s", step, hipGetErrorString(e));
     for (int q = 0; q < P; ++q) {
@@ -470,7 +591,7 @@ int fast_search(const as_trace_t* trace, const as_models_t* models, const int64_
       }
       int gstar = -1;
       for (int g = 0; g < pr.G; ++g)
-        if (fits(pr, sel, w, mstar, g) && (gstar < 0 || busy[(size_t)q * G + g] < busy[(size_t)q * G + gstar]))
+        if (fits(pr, sel, w, mstar, g) && (gstar < 0 || busy[brow[q] + g] < busy[brow[q] + gstar]))
           gstar = g;
       sel.mask[mstar] |= 1ull << gstar;
       sel.used[gstar] += w[mstar];

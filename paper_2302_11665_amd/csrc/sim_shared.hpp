@@ -306,9 +306,29 @@ __host__ __device__ constexpr size_t shared_stats_lds_bytes(int W, int M) {
 
 // Jobs of workgroup b: wavefront v holds jobs b*kWaves*JW + v*JW + lane/W,
 // JW = 64/W.  Per-request output rows must hold -2 when the kernel starts.
-template <int W, int SMAX, bool USIG, bool STATS = false>
-__global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
-  if (a.gate && *a.gate == 0) return;
+// The jobs one launch (or one shape segment of a multi-shape launch) runs:
+// their count, group-row stride, placement rows and outputs.
+struct JobSet {
+  int64_t J;
+  int32_t G;
+  const int32_t* group_cfg;
+  const uint64_t* host_mask;
+  int64_t* out_served;
+  double* out_attain;
+  uint64_t* out_digest;
+  int64_t* out_model_served;
+  double* out_group_busy;
+};
+
+__device__ __forceinline__ JobSet job_set(const KArgs& a) {
+  return JobSet{a.J, a.G, a.group_cfg, a.host_mask, a.out_served, a.out_attain, a.out_digest,
+                a.out_model_served, a.out_group_busy};
+}
+
+// One workgroup (block number blk of its job set) of the shared-trace
+// simulation.  ROWS: the launch may carry per-request output rows.
+template <int W, int SMAX, bool USIG, bool STATS, bool ROWS>
+__device__ __forceinline__ void shared_body(const KArgs& a, const JobSet& v, int64_t blk) {
   constexpr int JW = 64 / W;
   constexpr int kSlots = JW * kWaves;
   constexpr int RSH = rec_shift(SMAX);
@@ -325,8 +345,8 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int seg_lane = lane & (W - 1);
-  const int64_t job = (int64_t)blockIdx.x * kSlots + wave * JW + lane / W;
-  const bool job_ok = job < a.J;
+  const int64_t job = blk * kSlots + wave * JW + lane / W;
+  const bool job_ok = job < v.J;
 
   SharedConst c;
   int p = 0;
@@ -336,24 +356,24 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
     c.sigma = a.slo_scale[job % a.K];
   }
   int cfg = -1;
-  if (job_ok && seg_lane < a.G) cfg = a.group_cfg[(int64_t)p * a.G + seg_lane];
+  if (job_ok && seg_lane < v.G) cfg = v.group_cfg[(int64_t)p * v.G + seg_lane];
   if (cfg >= a.C || cfg < 0) cfg = -1;
   uint64_t hostbits = 0;  // bit m: this lane's group hosts model m
   if (cfg >= 0) {
-    const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
+    const uint64_t* hm = v.host_mask + (int64_t)p * a.M;
     for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> seg_lane) & 1u) << m;
   }
   int frow = -1;  // per-request output row of this job, -1 if none
-  if (job_ok)
+  if (ROWS && job_ok)
     for (int f = 0; f < a.n_finish; ++f)
       if (a.finish_jobs[f] == job) {
         frow = f;
         break;
       }
   c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
-  c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.n);
+  c.frowp = ROWS ? a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.n) : nullptr;
   c.flimit = a.n;
-  const bool wave_finish = c.fmask != 0;
+  const bool wave_finish = ROWS && c.fmask != 0;
   // a wavefront with per-request output has more to issue per request than
   // the others and sets the launch time: let it issue first on its SIMD
   if (wave_finish) __builtin_amdgcn_s_setprio(3);
@@ -431,13 +451,13 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
       else
         fast_chunk<W, SMAX, USIG, false, false, false, true>(st, c, sTD, sO, cnt, base, n);
     } else if (uni) {
-      if (wave_finish)
-        fast_chunk<W, SMAX, USIG, true, false, true>(st, c, sTD, sO, cnt, base, n);
+      if (ROWS && wave_finish)
+        fast_chunk<W, SMAX, USIG, ROWS, false, true>(st, c, sTD, sO, cnt, base, n);
       else
         fast_chunk<W, SMAX, USIG, false, false, true>(st, c, sTD, sO, cnt, base, n);
     } else {
-      if (wave_finish)
-        fast_chunk<W, SMAX, USIG, true, false, false>(st, c, sTD, sO, cnt, base, n);
+      if (ROWS && wave_finish)
+        fast_chunk<W, SMAX, USIG, ROWS, false, false>(st, c, sTD, sO, cnt, base, n);
       else
         fast_chunk<W, SMAX, USIG, false, false, false>(st, c, sTD, sO, cnt, base, n);
     }
@@ -445,19 +465,39 @@ __global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
 
   const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum);
   if (job_ok && seg_lane == 0) {
-    a.out_served[job] = (int64_t)st.served;
-    if (a.out_attain) a.out_attain[job] = n > 0 ? (double)st.served / (double)n : 0.0;
-    if (a.out_digest) {
-      a.out_digest[2 * job] = st.hash;
-      a.out_digest[2 * job + 1] = fin_sum;
+    v.out_served[job] = (int64_t)st.served;
+    if (v.out_attain) v.out_attain[job] = n > 0 ? (double)st.served / (double)n : 0.0;
+    if (v.out_digest) {
+      v.out_digest[2 * job] = st.hash;
+      v.out_digest[2 * job + 1] = fin_sum;
     }
   }
   if constexpr (STATS) {
-    if (job_ok && seg_lane < a.G && a.out_group_busy) a.out_group_busy[job * a.G + seg_lane] = st.busy;
-    if (job_ok && a.out_model_served)
-      for (int m = seg_lane; m < a.M; m += W) a.out_model_served[job * a.M + m] = (int64_t)c.cnt[m];
+    if (job_ok && seg_lane < v.G && v.out_group_busy) v.out_group_busy[job * v.G + seg_lane] = st.busy;
+    if (job_ok && v.out_model_served)
+      for (int m = seg_lane; m < a.M; m += W) v.out_model_served[job * a.M + m] = (int64_t)c.cnt[m];
   }
 }
+
+template <int W, int SMAX, bool USIG, bool STATS = false>
+__global__ __launch_bounds__(kThreads) void shared_kernel(const KArgs a) {
+  if (a.gate && *a.gate == 0) return;
+  shared_body<W, SMAX, USIG, STATS, true>(a, job_set(a), blockIdx.x);
+}
+
+// Multi-shape launches: consecutive block ranges run job sets of different
+// shapes (lanes per job 2^wl, padded stages 2^sl), so that the jobs of
+// several shapes share one dispatch instead of queueing behind each other.
+constexpr int kMaxShapeSegs = 16;
+struct ShapeSeg {
+  int32_t wl, sl;
+  int64_t block0;  // first block of the segment
+  JobSet v;
+};
+struct MultiSegs {
+  int32_t n;
+  ShapeSeg s[kMaxShapeSegs];
+};
 
 // ---------------------------------------------------------------------------
 // Segmented jobs with up to 64 groups: one job per wavefront (lane g = group

@@ -1318,17 +1318,46 @@ bool spec_pays(const KArgs& k, int nseg, int jpw, int per_cu) {
 // ALPASERVE_PATH=spec forces the kernels), or when the workspace would be too
 // large.  With can_give_up the workspace outlives the call: the caller's
 // gated fallback kernels read the give-up flag in it, then release it.
+namespace {
+
+// Whether the speculative kernels take the call (sizes, LDS, segments that
+// pay or are forced), with their LDS sizes, occupancy and segment count.
+bool spec_plan(const KArgs& k, int smax, size_t& lds_u, size_t& lds_g, int& per_cu, int& nseg) {
+  using namespace as_dev;
+  if (k.n <= 0 || k.J <= 0) return false;
+  const size_t lim = shared_lds_limit();
+  const int jpw = kSpecJobsPerWave;
+  lds_u = spec_lds_bytes(k.M, k.C, k.G, smax, true, jpw);
+  lds_g = spec_lds_bytes(k.M, k.C, k.G, smax, false, jpw);
+  if (lds_g > lim || lds_u > lim) return false;
+  per_cu = 1;
+  switch (smax) {
+    case 1: per_cu = spec_occupancy_mb<1>(k.G, lds_u); break;
+    case 2: per_cu = spec_occupancy_mb<2>(k.G, lds_u); break;
+    case 4: per_cu = spec_occupancy_mb<4>(k.G, lds_u); break;
+    default: per_cu = spec_occupancy_mb<8>(k.G, lds_u); break;
+  }
+  nseg = spec_segments(k.n, k.J, jpw, per_cu);
+  return spec_forced() || spec_pays(k, nseg, jpw, per_cu);
+}
+
+}  // namespace
+
+bool spec_takes(const KArgs& k, int smax) {
+  size_t lds_u = 0, lds_g = 0;
+  int per_cu = 1, nseg = 1;
+  return spec_plan(k, smax, lds_u, lds_g, per_cu, nseg);
+}
+
 int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void* caller_ws,
              size_t caller_ws_bytes, void** workspace, const int32_t** gave_up) {
   using namespace as_dev;
   *workspace = nullptr;
   *gave_up = nullptr;
-  if (k.n <= 0 || k.J <= 0) return AS_E_LIMITS;
-  const size_t lim = shared_lds_limit();
   const int jpw = kSpecJobsPerWave;
-  const size_t lds_u = spec_lds_bytes(k.M, k.C, k.G, smax, true, jpw);
-  const size_t lds_g = spec_lds_bytes(k.M, k.C, k.G, smax, false, jpw);
-  if (lds_g > lim || lds_u > lim) return AS_E_LIMITS;
+  size_t lds_u = 0, lds_g = 0;
+  int per_cu = 1, nseg = 1;
+  if (!spec_plan(k, smax, lds_u, lds_g, per_cu, nseg)) return AS_E_LIMITS;
 
   SpecArgs a;
   std::memset(&a, 0, sizeof a);
@@ -1354,15 +1383,7 @@ int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void* cal
   std::memcpy(a.cfg_stages, k.cfg_stages, sizeof a.cfg_stages);
   std::memcpy(a.finish_jobs, k.finish_jobs, sizeof a.finish_jobs);
   a.njb = (int32_t)((k.J + jpw - 1) / jpw);
-  int per_cu = 1;
-  switch (smax) {
-    case 1: per_cu = spec_occupancy_mb<1>(k.G, lds_u); break;
-    case 2: per_cu = spec_occupancy_mb<2>(k.G, lds_u); break;
-    case 4: per_cu = spec_occupancy_mb<4>(k.G, lds_u); break;
-    default: per_cu = spec_occupancy_mb<8>(k.G, lds_u); break;
-  }
-  a.nseg = spec_segments(k.n, k.J, jpw, per_cu);
-  if (!spec_forced() && !spec_pays(k, a.nseg, jpw, per_cu)) return AS_E_LIMITS;
+  a.nseg = nseg;
   a.warmup = kSpecWarmup;
   if (const char* w = getenv("ALPASERVE_SPEC_WARMUP")) a.warmup = std::max<int64_t>(0, atoll(w));
   a.ck = kSpecCheckpoint;
