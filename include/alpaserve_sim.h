@@ -155,6 +155,11 @@ typedef struct {
  *   out_finish       [n_finish][finish_stride]; row f receives job
  *                    finish_jobs[f]'s outputs for requests i < min(segment
  *                    length, finish_stride)
+ * Asynchronous on `stream`.  With more than 32 groups (one job per
+ * wavefront) and 2..4096 jobs, the jobs are launched longest and shortest
+ * segment alternating, which changes no result; the order array (4 bytes
+ * per job) comes from the library's memory pool and is released
+ * stream-ordered.
  */
 int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,
                      int32_t n_segments, const as_models_t* models,

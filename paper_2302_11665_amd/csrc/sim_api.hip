@@ -563,6 +563,69 @@ int as_simulate_placements_noalloc(const as_trace_t* trace, const as_models_t* m
                              out_digest, finish_jobs, n_finish, out_finish, stream, true);
 }
 
+namespace as_dev {
+namespace {
+
+constexpr int kOrderMaxJobs = 4096;  // jobs the one-workgroup sort below takes
+
+// Launch order of the one-job-per-wavefront kernel: the jobs sorted by
+// segment length (longest first, lower index first on ties), then the
+// longest and the shortest alternating -- order[2i] the i-th longest,
+// order[2i + 1] the i-th shortest -- so that the longest chains share their
+// SIMDs with short ones.  One workgroup of 1024 threads, J <= 4096.
+__global__ __launch_bounds__(1024) void seg_order(const KArgs a, int32_t* __restrict__ order) {
+  __shared__ int64_t key[kOrderMaxJobs];
+  __shared__ int32_t val[kOrderMaxJobs];
+  const int J = (int)a.J;
+  int P = 1;
+  while (P < J) P <<= 1;
+  for (int i = threadIdx.x; i < P; i += blockDim.x) {
+    int64_t len = -1;  // padding sorts after every job
+    if (i < J) {
+      const as_job_t jb = a.jobs[i];
+      len = 0;
+      if (jb.placement >= 0 && jb.placement < a.P && jb.segment >= 0 && jb.segment < a.n_segments) {
+        const int64_t total = a.seg_off[a.n_segments];
+        int64_t b = a.seg_off[jb.segment], e = a.seg_off[jb.segment + 1];
+        b = b < 0 ? 0 : (b > total ? total : b);
+        e = e < b ? b : (e > total ? total : e);
+        len = e - b;
+      }
+    }
+    key[i] = len;
+    val[i] = i;
+  }
+  __syncthreads();
+  // bitonic sort: descending length, ascending index on ties
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < P; i += blockDim.x) {
+        const int l = i ^ j;
+        if (l > i) {
+          const bool before = key[i] > key[l] || (key[i] == key[l] && val[i] < val[l]);  // i precedes l
+          const bool desc = (i & k) == 0;
+          if (desc != before) {
+            const int64_t tk = key[i];
+            key[i] = key[l];
+            key[l] = tk;
+            const int32_t tv = val[i];
+            val[i] = val[l];
+            val[l] = tv;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < J; i += blockDim.x) {
+    const int h = i >> 1;
+    order[i] = (i & 1) == 0 ? val[h] : val[J - 1 - h];
+  }
+}
+
+}  // namespace
+}  // namespace as_dev
+
 int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,
                      int32_t n_segments, const as_models_t* models,
                      const as_placements_t* placements, const as_job_t* jobs, int32_t n_jobs,
@@ -606,8 +669,24 @@ int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_o
       if ((e = hipGetLastError()) != hipSuccess)
         return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     }
+    // long and short chains interleaved (skipped, never an error, where the
+    // jobs are too many for the sort or its array cannot be allocated)
+    int32_t* order = nullptr;
+    if (n_jobs >= 2 && n_jobs <= as_dev::kOrderMaxJobs &&
+        pool_alloc(reinterpret_cast<void**>(&order), (size_t)n_jobs * 4, s) == hipSuccess) {
+      hipLaunchKernelGGL(as_dev::seg_order, dim3(1), dim3(1024), 0, s, a, order);
+      if ((e = hipGetLastError()) != hipSuccess) {
+        (void)hipFreeAsync(order, s);
+        return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+      }
+      a.order = order;
+    } else {
+      (void)hipGetLastError();
+    }
     e = as_host::launch_seg64(smax, a, lds_seg, s);
+    const hipError_t ef = order ? hipFreeAsync(order, s) : hipSuccess;
     if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+    if (ef != hipSuccess) return fail(AS_E_HIP, "order release failed: %s", hipGetErrorString(ef));
     return ok();
   }
   int GPL = 1;

@@ -566,8 +566,8 @@ extern "C" int as_simulate_batched(const as_trace_t* trace, const as_models_t* m
   const size_t o_blk = 256, o_off = o_blk + up((size_t)la.nblk * ka.M * 4), o_ord = o_off + up((size_t)(ka.M + 1) * 4),
                o_lt = o_ord + up(n * 4), o_li = o_lt + up(n * 8), o_mix = o_li + up(n * 4), total = o_mix + up(n * 8);
   unsigned char* ws = nullptr;
-  hipError_t e = hipMallocAsync((void**)&ws, total, s);
-  if (e != hipSuccess) return fail(AS_E_NOMEM, "hipMallocAsync(%zu): %s", total, hipGetErrorString(e));
+  hipError_t e = pool_alloc(reinterpret_cast<void**>(&ws), total, s);
+  if (e != hipSuccess) return fail(AS_E_NOMEM, "device allocation of %zu bytes: %s", total, hipGetErrorString(e));
   a.flags = reinterpret_cast<uint32_t*>(ws);
   la.flags = a.flags;
   la.blk = reinterpret_cast<uint32_t*>(ws + o_blk);

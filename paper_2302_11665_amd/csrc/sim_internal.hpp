@@ -20,6 +20,10 @@ int ok();
 int pow2ceil(int x);
 // LDS a workgroup may use on the current device (160 KiB on gfx950).
 size_t shared_lds_limit();
+// Stream-ordered device allocation from the library's private memory pool
+// (one per device, memory kept for reuse between calls); release with
+// hipFreeAsync on a stream ordered after the last use.
+hipError_t pool_alloc(void** p, size_t bytes, hipStream_t s);
 // Checks shared by the simulate entry points; fill the model and placement
 // part of a (placement arrays may be set later by the caller) and return the
 // group count in W and the padded stage count in smax.

@@ -60,6 +60,7 @@ struct KArgs {
   int64_t n;               // shared trace length
   const int64_t* seg_off;  // segmented: [n_segments + 1]
   const as_job_t* jobs;    // segmented: [J]
+  const int32_t* order;    // segmented, one job per wavefront: slot -> job, a permutation (null: identity)
   const double* d_single;
   const double* stage_lat;
   const int32_t* group_cfg;

@@ -538,8 +538,9 @@ __device__ __forceinline__ void seg_job(const KArgs& a, int64_t j, int& p, doubl
   len = e - b;
 }
 
-// Job j = blockIdx.x * kWaves + wavefront.  Per-request output rows must hold
-// -2 over [0, min(segment length, finish_stride)) when the kernel starts.
+// Slot blockIdx.x * kWaves + wavefront runs job order[slot] (the slot itself
+// without an order).  Per-request output rows must hold -2 over
+// [0, min(segment length, finish_stride)) when the kernel starts.
 template <int SMAX>
 __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   constexpr int W = 64;
@@ -556,8 +557,9 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int64_t job = (int64_t)blockIdx.x * kWaves + wave;
-  const bool job_ok = job < a.J;
+  const int64_t slot = (int64_t)blockIdx.x * kWaves + wave;
+  const bool job_ok = slot < a.J;
+  const int64_t job = job_ok && a.order ? (int64_t)a.order[slot] : slot;
   double* sTD = sTDall + (size_t)wave * 2 * kSegChunk;
   uint32_t* sO = sOall + (size_t)wave * kSegChunk;
 
@@ -632,6 +634,7 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
   st.fin_sum = st.hash = st.served = 0;
   st.wlo = 0;
+  st.busy = 0.0;
 
   for (int64_t base = 0; base < n_job; base += kSegChunk) {
     const int cnt = (int)((n_job - base) < kSegChunk ? (n_job - base) : kSegChunk);

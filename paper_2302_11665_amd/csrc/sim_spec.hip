@@ -1229,12 +1229,25 @@ int compute_units() {
   return cache[dev];
 }
 
+
+// warm-up requests before a segment (measured on the 8192-placement workload:
+// 32768 -> 255.7 ms per step, 16384 -> 249.5, 8192 -> 242-244, 2048 -> 251,
+// none -> 261: a shorter warm-up leaves more to the rounds)
+constexpr int64_t kSpecWarmup = 8192;
+// requests per segment at least: the warm-up and the rounds' re-runs stay a
+// small part of a segment's work (shorter traces, like the searches' 151k
+// requests, ran slower on these kernels)
+constexpr int64_t kSpecMinSegment = 131072;
+constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
+
+}  // namespace
+
 // Stream-ordered workspace allocation from a memory pool private to this
 // library, one per device, whose release threshold is at its maximum: the
 // workspace freed by one call is reused by the next instead of going back to
 // the driver, and the process's default pool keeps its own settings.  Where a
 // private pool cannot be created, the default pool serves as it is.
-hipError_t spec_alloc(void** p, size_t bytes, hipStream_t s) {
+hipError_t pool_alloc(void** p, size_t bytes, hipStream_t s) {
   static std::mutex mu;
   static hipMemPool_t pools[64];
   static int state[64] = {0};  // 0 not tried, 1 private pool, 2 default pool
@@ -1263,18 +1276,6 @@ hipError_t spec_alloc(void** p, size_t bytes, hipStream_t s) {
   }
   return st == 1 ? hipMallocFromPoolAsync(p, bytes, pools[dev], s) : hipMallocAsync(p, bytes, s);
 }
-
-// warm-up requests before a segment (measured on the 8192-placement workload:
-// 32768 -> 255.7 ms per step, 16384 -> 249.5, 8192 -> 242-244, 2048 -> 251,
-// none -> 261: a shorter warm-up leaves more to the rounds)
-constexpr int64_t kSpecWarmup = 8192;
-// requests per segment at least: the warm-up and the rounds' re-runs stay a
-// small part of a segment's work (shorter traces, like the searches' 151k
-// requests, ran slower on these kernels)
-constexpr int64_t kSpecMinSegment = 131072;
-constexpr int64_t kSpecCheckpoint = 8192;   // requests between saved states
-
-}  // namespace
 
 // Segments per job for the speculative path: enough (job block, segment)
 // wavefronts to fill the device at the occupancy the LDS allows, each segment
@@ -1421,7 +1422,7 @@ int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void* cal
     // the kernels that need none
     size_t free_b = 0, total_b = 0;
     if (hipMemGetInfo(&free_b, &total_b) != hipSuccess || total > total_b / 4) return AS_E_LIMITS;
-    e = spec_alloc(reinterpret_cast<void**>(&ws), total, stream);
+    e = pool_alloc(reinterpret_cast<void**>(&ws), total, stream);
     if (e != hipSuccess || !ws)
       return fail(AS_E_NOMEM, "workspace of %zu bytes: %s", total, hipGetErrorString(e));
   }
