@@ -3,8 +3,9 @@ oracle, bit-exact: served counts, the order-free digest and every
 per-request finish time, for 1 to 64 groups, 1 to 8 stages, several maximum
 batch sizes, latency slopes and SLO scales (0 and +inf included), ragged
 traces, and the batching experiment's workload shape (16 models on groups of
-4 devices, a bursty Gamma trace, batch sizes 1-8 at slope 1), plus a queue
-overflow that must be reported rather than ignored."""
+4 devices, a bursty Gamma trace, batch sizes 1-8 at slope 1), batches larger
+than a wavefront (the batch size is searched 64 sizes at a time), plus a
+queue overflow that must be reported rather than ignored."""
 import os
 import sys
 
@@ -139,3 +140,24 @@ def test_batching_empty_and_overflow(dev):
     s, dg, ofin, _ = oracle.lib().simulate_job_batched(tb, mb, np.ones(1), np.array([1], np.int32), np.ones((1, 1, 1)),
                                                        np.zeros(1, np.int32), np.ones(1, np.uint64), INF, 4, 1.0)
     assert int(served[0]) == s == 300 and fin[0].tobytes() == ofin.tobytes()
+
+
+@pytest.mark.parametrize("B", [64, 65, 100, 150])
+def test_batching_large_batches(dev, B):
+    """Bursts that queue hundreds of requests with a slope small enough that
+    batches of more than 64 requests meet the SLO: the largest fitting
+    batch is found 64 sizes per pass, and the first size that misses ends
+    the search, as a size-by-size search would."""
+    rng = np.random.default_rng(40 + B)
+    n = 900
+    t = np.sort(np.concatenate([np.zeros(300), rng.uniform(0.0, 30.0, n - 300)]))
+    model = rng.integers(0, 3, n).astype(np.int32)
+    cs = np.array([2], np.int32)
+    L = rng.uniform(0.05, 0.2, (3, 1, 2))
+    d = L[:, 0, :].sum(axis=1)
+    gc = np.zeros((2, 2), np.int32)
+    hm = np.array([[1, 1, 2], [3, 2, 1]], np.uint64)
+    scales = [4.0, 40.0, INF]
+    say("large batches B", B)
+    served, digest, fin = _run(dev, t, model, d, cs, L, gc, hm, scales, B, 0.002, [1, 5], qcap=1024)
+    _check(oracle.lib(), t, model, d, cs, L, gc, hm, scales, B, 0.002, served, digest, fin, [1, 5])

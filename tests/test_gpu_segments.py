@@ -130,3 +130,30 @@ def test_random_segmented_jobs(dev, G):
         stride = int(rng.choice([50, 4000]))
         say("segmented", G, S, "jobs", J, "requests", len(c["t"]), "stride", stride)
         _check(c, _run(dev, c, finish, stride), finish, stride)
+
+
+def _permuted(c, perm):
+    return dict(c, jp=c["jp"][perm], js=c["js"][perm], jsc=c["jsc"][perm])
+
+
+@pytest.mark.parametrize("J", [2, 300, 4100])
+def test_launch_order_does_not_change_results(dev, J):
+    """With more than 32 groups the jobs run one per wavefront, launched
+    longest and shortest segment alternating (sorted on the device for up
+    to 4096 jobs, in the given order beyond): the results, indexed by job,
+    are the same for any order of the job records."""
+    rng = np.random.default_rng(900 + J)
+    c = _case(rng, 64, 2)
+    n_seg = len(c["offs"]) - 1
+    # many jobs over segments of very different lengths (several ties)
+    c = dict(c, jp=rng.integers(0, c["gcfg"].shape[0], J).astype(np.int32),
+             js=rng.integers(0, n_seg, J).astype(np.int32), jsc=rng.choice([0.5, 2.0, 5.0, np.inf], J))
+    say("launch order", J, "jobs", n_seg, "segments")
+    ref = _run(dev, c, [], 0)
+    perm = rng.permutation(J)
+    got = _run(dev, _permuted(c, perm), [], 0)
+    for a, b in zip(ref[:3], got[:3]):
+        assert np.array_equal(np.asarray(a)[perm], np.asarray(b))
+    sample = sorted(set(rng.choice(J, size=min(J, 24), replace=False).tolist()))
+    sub = dict(c, jp=c["jp"][sample], js=c["js"][sample], jsc=c["jsc"][sample])
+    _check(sub, tuple(np.asarray(x)[sample] for x in ref[:3]) + (None,), [], 0)
