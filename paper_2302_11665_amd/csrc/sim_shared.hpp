@@ -589,6 +589,8 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.finish_stride);
   c.flimit = n_job < a.finish_stride ? n_job : a.finish_stride;
   const bool wave_finish = c.fmask != 0;
+  // whether the row is shorter than the segment (else no per-request limit test)
+  const bool row_lim = c.flimit < n_job;
   if (wave_finish) __builtin_amdgcn_s_setprio(3);
   const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
   const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
@@ -653,15 +655,19 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (uni) {
-      if (wave_finish)
+      if (wave_finish && row_lim)
         fast_chunk<W, SMAX, true, true, true, true>(st, c, sTD, sO, cnt, base, n_job);
+      else if (wave_finish)
+        fast_chunk<W, SMAX, true, true, false, true>(st, c, sTD, sO, cnt, base, n_job);
       else
-        fast_chunk<W, SMAX, true, false, true, true>(st, c, sTD, sO, cnt, base, n_job);
+        fast_chunk<W, SMAX, true, false, false, true>(st, c, sTD, sO, cnt, base, n_job);
     } else {
-      if (wave_finish)
+      if (wave_finish && row_lim)
         fast_chunk<W, SMAX, true, true, true, false>(st, c, sTD, sO, cnt, base, n_job);
+      else if (wave_finish)
+        fast_chunk<W, SMAX, true, true, false, false>(st, c, sTD, sO, cnt, base, n_job);
       else
-        fast_chunk<W, SMAX, true, false, true, false>(st, c, sTD, sO, cnt, base, n_job);
+        fast_chunk<W, SMAX, true, false, false, false>(st, c, sTD, sO, cnt, base, n_job);
     }
   }
 
