@@ -60,20 +60,20 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "68bbf8c83e6b92df8a04e294ead0d5832fb298096657f926cfc8e127af8eab29",
+    "sources_sha256": "22d04c901a3d43cc0c6c447f311638840be2e6fbf1156ecef56136ed0c192b60",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
     "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check "
               "(+ the pass-0 variants that return at once)",
-    "fetch_kib": 2160172.31, "write_kib": 5990877.62,
-    "fetch_scale": 1048576.0 / 524302.04, "write_scale": 1048576.0 / 1048576.0,
+    "fetch_kib": 2160561.94, "write_kib": 5990875.75,
+    "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "68bbf8c83e6b92df8a04e294ead0d5832fb298096657f926cfc8e127af8eab29",
+    "sources_sha256": "22d04c901a3d43cc0c6c447f311638840be2e6fbf1156ecef56136ed0c192b60",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595583.44, "write_kib": 14016.75,
-    "fetch_scale": 1048576.0 / 524302.04, "write_scale": 1048576.0 / 1048576.0,
+    "fetch_kib": 2595574.44, "write_kib": 14016.72,
+    "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
 }
 
 
