@@ -401,11 +401,23 @@ def bench_search(args, np, torch, sim, problems):
         from concurrent.futures import ThreadPoolExecutor
         from oracle import greedy as og
         lib = oracle.lib()
-        with ThreadPoolExecutor(min(host_threads(), len(gp.partitions))) as ex:
-            fs = list(ex.map(lambda part: og.fast_selection(lib, gp.t, gp.model, gp.d_single, gp.weight_mib,
-                                                            gp.cfg_stages, gp.stage_lat, part["group_cfg"],
-                                                            part["group_mem_mib"], gp.slo_scale)["best_served"],
-                             gp.partitions))
+
+        def one(part):
+            t1 = time.perf_counter()
+            b = og.fast_selection(lib, gp.t, gp.model, gp.d_single, gp.weight_mib, gp.cfg_stages, gp.stage_lat,
+                                  part["group_cfg"], part["group_mem_mib"], gp.slo_scale)["best_served"]
+            return b, time.perf_counter() - t1
+
+        nthr = min(host_threads(), len(gp.partitions))
+        t1 = time.perf_counter()
+        with ThreadPoolExecutor(nthr) as ex:
+            got = list(ex.map(one, gp.partitions))
+        fs = [b for b, _ in got]
+        # the oracle's C simulation releases the GIL: the partitions' times add
+        # up to what one thread would take
+        fh["oracle_wall_s"] = round(time.perf_counter() - t1, 3)
+        fh["oracle_threads"] = nthr
+        fh["oracle_one_thread_s"] = round(sum(x for _, x in got), 3)
         fh["oracle_heuristic_served_by_partition"] = fs
         fh["ratio_by_partition"] = [round(a / b, 5) if b else None for a, b in zip(fs, gs)]
         fh["parity"] = max(fs) == r["served"]
