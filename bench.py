@@ -60,7 +60,7 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "22d04c901a3d43cc0c6c447f311638840be2e6fbf1156ecef56136ed0c192b60",
+    "sources_sha256": "18f1a94944a2b739fb15cf38b2485210e3c095539eda4de69f6e3cd45694e7e4",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, digest):
     # its counters summed over the step's dispatches
@@ -70,7 +70,7 @@ MEASURED_TRAFFIC = {
     "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "22d04c901a3d43cc0c6c447f311638840be2e6fbf1156ecef56136ed0c192b60",
+    "sources_sha256": "18f1a94944a2b739fb15cf38b2485210e3c095539eda4de69f6e3cd45694e7e4",
     "kernel": "seg_kernel<1>",
     "fetch_kib": 2595574.44, "write_kib": 14016.72,
     "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,

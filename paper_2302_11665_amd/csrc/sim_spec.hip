@@ -1422,6 +1422,11 @@ int run_spec(KArgs& k, int smax, hipStream_t stream, bool can_give_up, void* cal
     // the kernels that need none
     size_t free_b = 0, total_b = 0;
     if (hipMemGetInfo(&free_b, &total_b) != hipSuccess || total > total_b / 4) return AS_E_LIMITS;
+    // ALPASERVE_SPEC_MAX_WORKSPACE (bytes) makes a larger workspace fail as a
+    // failed allocation does (tests of the fallback to the other kernels)
+    if (const char* cap = getenv("ALPASERVE_SPEC_MAX_WORKSPACE"))
+      if ((long long)total > atoll(cap))
+        return fail(AS_E_NOMEM, "workspace of %zu bytes above ALPASERVE_SPEC_MAX_WORKSPACE", total);
     e = pool_alloc(reinterpret_cast<void**>(&ws), total, stream);
     if (e != hipSuccess || !ws)
       return fail(AS_E_NOMEM, "workspace of %zu bytes: %s", total, hipGetErrorString(e));
