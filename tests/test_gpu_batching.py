@@ -161,3 +161,17 @@ def test_batching_large_batches(dev, B):
     say("large batches B", B)
     served, digest, fin = _run(dev, t, model, d, cs, L, gc, hm, scales, B, 0.002, [1, 5], qcap=1024)
     _check(oracle.lib(), t, model, d, cs, L, gc, hm, scales, B, 0.002, served, digest, fin, [1, 5])
+
+
+def test_batching_every_lane_twice(dev):
+    """64 groups and 64 models: every lane holds a group's free times and a
+    model's queue at once."""
+    rng = np.random.default_rng(64)
+    G, M, n = 64, 64, 3000
+    t, model, d, cs, L, gc, hm = _case(rng, G, 2, M, n, P=2)
+    # bursts, so that queues form on many models at once
+    t = np.sort(np.concatenate([t[: n // 2], np.repeat(rng.uniform(0, t[-1], 15), 100)]))[:n]
+    scales = [3.0, INF]
+    say("every lane twice", G, M, n)
+    served, digest, fin = _run(dev, t, model, d, cs, L, gc, hm, scales, 4, 0.5, [0, 3])
+    _check(oracle.lib(), t, model, d, cs, L, gc, hm, scales, 4, 0.5, served, digest, fin, [0, 3])

@@ -136,7 +136,7 @@ def _permuted(c, perm):
     return dict(c, jp=c["jp"][perm], js=c["js"][perm], jsc=c["jsc"][perm])
 
 
-@pytest.mark.parametrize("J", [2, 300, 4100])
+@pytest.mark.parametrize("J", [2, 300, 4096, 4100])
 def test_launch_order_does_not_change_results(dev, J):
     """With more than 32 groups the jobs run one per wavefront, launched
     longest and shortest segment alternating (sorted on the device for up
