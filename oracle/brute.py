@@ -128,13 +128,17 @@ def _mix64(z):
 
 
 def simulate_batched(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_mask, slo_scale,
-                     max_batch, beta):
+                     max_batch, beta, on_queue=None):
     """Dynamic batching (Sec. 6.5) as an event-driven simulation: a global clock
     walks through arrival events and group-idle events; every group keeps the
     list of batches it ran, and its stage timelines come from replaying them
     through explicit stage servers (a batch is one unit whose stage latencies
     are the model's times (1 + beta (b - 1))).  Rules as in the C oracle's
-    batched simulation.  Returns (served, finish[n], batch[n], digest)."""
+    batched simulation.  Returns (served, finish[n], batch[n], digest).
+    on_queue(m, queue, i, at_once), if given, sees model m's queue (trace
+    indices) at each hosted arrival i: after the request joins it, or, when
+    the request runs (or is dropped) at once, as it stands (it changes
+    nothing)."""
     t = [float(x) for x in t]
     model = [int(x) for x in model]
     n, G = len(t), len(group_cfg)
@@ -206,6 +210,8 @@ def simulate_batched(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_
         if int(host_mask[m]) != 0:
             avail = [(free0(g), g) for g in range(G) if hosts(m, g) and free0(g) <= t[i]]
             if avail:
+                if on_queue:
+                    on_queue(m, tuple(queue[m]), i, True)
                 _, g = min(avail)
                 fin = run(g, m, 1, t[i])
                 if not fin > t[i] + float(slo_scale) * float(d_single[m]):
@@ -214,6 +220,8 @@ def simulate_batched(t, model, d_single, cfg_stages, stage_lat, group_cfg, host_
                     batch[i] = 1
             else:
                 queue[m].append(i)
+                if on_queue:
+                    on_queue(m, tuple(queue[m]), i, False)
         i += 1
     served = int((batch > 0).sum())
     h = 0

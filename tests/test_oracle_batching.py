@@ -131,3 +131,30 @@ def test_invariants(olib):
             assert len(members) % b == 0
         assert h == sum(_mix64(int(i)) for i in np.nonzero(served)[0]) % (1 << 64)
         assert fs == int(fin[served].view(np.uint64).astype(object).sum()) % (1 << 64)
+
+
+def test_queue_is_a_run_of_its_models_arrivals():
+    """A model's queue is always a run of its arrivals in trace order (the
+    GPU kernel keeps queues as two positions in per-model arrival lists on
+    this ground): a hosted arrival that runs or is dropped at once finds its
+    model's queue empty, since the idle events before it let every group
+    with queued work take it; and when request i joins the queue of model m,
+    the queue holds exactly the arrivals of m from its head to i, since
+    requests leave a queue only at its head."""
+    rng = np.random.default_rng(91)
+    long_runs = 0
+    for k in range(400):
+        t, model, d, cs, L, gc, hm, sigma = _case(rng, n=int(rng.integers(5, 40)), dyadic=k % 2 == 0)
+        B = int(rng.choice([1, 2, 3, 8]))
+        beta = float(rng.choice([0.0, 0.25, 1.0]))
+
+        def check(m, q, i, at_once):
+            nonlocal long_runs
+            if at_once:
+                assert q == (), (k, m, q, i)
+            else:
+                assert list(q) == [j for j in range(q[0], i + 1) if model[j] == m], (k, m, q, i)
+                long_runs += len(q) >= 3
+
+        brute.simulate_batched(t, model, d, cs, L, gc, hm, sigma, B, beta, on_queue=check)
+    assert long_runs > 50  # queues of several requests were seen
