@@ -592,13 +592,13 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
 
 __device__ __forceinline__ int spec_ckpts(int64_t b, int64_t e, int64_t ck) { return (int)((e - b - 1) / ck); }
 
-// Pass 0 of one wavefront; ROWS: some lane of it writes finish rows.
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL, bool ROWS>
+// Pass 0 of one wavefront (the per-request output rows are written by
+// spec_rows once the rounds have made every saved state exact).
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
 __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, int lane, int k,
                                                 const SpecLane& ln, int c0) {
   LaneMasks<MB> msk;
   (void)msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-  const bool wave_rows = ROWS;
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int GS = a.G * SMAX;
   if (lane < JPW)
@@ -617,11 +617,10 @@ __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, 
   const size_t seg_base = ((size_t)k * GS) * J + ln.job;
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
-  bool rows_now = false;  // this chunk lies in the segment and the wavefront has finish rows
   const size_t ck0 = (size_t)k * a.ckps;
   if (w0 == b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA, FULL, ROWS>(
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, FULL, false>(
       a, s, msk, ln, lane, S0, w0, e, on,
       [&](int64_t cb) {
         if (cb == b) {
@@ -629,7 +628,6 @@ __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, 
           served = 0;
           fsum = 0;
         }
-        rows_now = wave_rows && cb >= b;
         if (cb == b && w0 < b && ln.valid)
           for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = s.F[q * JPW + lane];
         if (cb > b && (cb - b) % a.ck == 0 && ln.valid) {
@@ -638,12 +636,14 @@ __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, 
           a.ck_served[j * J + ln.job] = served;
           a.ck_fsum[j * J + ln.job] = fsum;
         }
-        return rows_now ? 2 : 1;
+        return 1;
       },
       [&](int64_t i, int r, double out, bool sv, bool rows) {
+        (void)i;
+        (void)r;
+        (void)rows;
         fsum += sv ? bits_of(out) : 0;
         word = push_bit(word, sv);
-        if (rows && ln.frow >= 0) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [&](int64_t cb, int cnt) {
         word = chunk_word(word, cnt);
@@ -688,13 +688,62 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
     const bool many = m0.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
     if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
   }
-  // the wavefronts with finish rows (few) run their own copy of the loop,
-  // so that the others carry no per-request code for the rows
-  if (__builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0) {
-    spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL, true>(a, lds, lane, k, ln, c0);
-  } else {
-    spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL, false>(a, lds, lane, k, ln, c0);
+  spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL>(a, lds, lane, k, ln, c0);
+}
+
+// Per-request output rows of the jobs that have one.  Pass 0 and the rounds
+// write none: once the rounds are done, every saved state is the exact state
+// at its point of the trace (a segment's start, and every ck requests into
+// it), so each piece of ck requests is simulated again from the state before
+// it, all pieces at once, and only the rows are written.  Lanes are jobs with
+// a row (JPW per wavefront); blocks are row blocks x segments x pieces, and a
+// piece past its segment's end returns at once.
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
+__global__ __launch_bounds__(64) void spec_rows(const SpecArgs a) {
+  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels write the rows
+  if ((a.cfg_info[0] != 0) != UCFG) return;
+  const int c0 = UCFG ? a.cfg_info[1] : 0;
+  extern __shared__ double lds[];
+  const int lane = threadIdx.x;
+  const int nrb = (a.n_finish + JPW - 1) / JPW;
+  const int np = a.ckps + 1;
+  const int rb = blockIdx.x % nrb;
+  const int pc = (blockIdx.x / nrb) % np;
+  const int k = blockIdx.x / (nrb * np);
+  const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
+  const int64_t pb = b + (int64_t)pc * a.ck;
+  if (pb >= e) return;
+  const int64_t pe = e - pb < a.ck ? e : pb + a.ck;
+  SpecLane ln;
+  const int f = rb * JPW + lane;
+  ln.valid = lane < JPW && f < a.n_finish;
+  ln.job = ln.valid ? a.finish_jobs[f] : 0;
+  ln.p = ln.valid ? ln.job / a.K : 0;
+  ln.scale = ln.valid ? a.slo_scale[ln.job % a.K] : 0.0;
+  ln.frow = ln.valid ? f : -1;
+  LaneMasks<MB> msk;
+  {
+    const bool many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+    if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
   }
+  const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
+  const int GS = a.G * SMAX;
+  const int64_t J = a.J;
+  if (lane < JPW)
+    for (int q = 0; q < GS; ++q)
+      s.F[q * JPW + lane] = !ln.valid ? 0.0
+                            : pc == 0 ? a.st_start[((size_t)k * GS + q) * J + ln.job]
+                                      : a.ckpt[(((size_t)k * a.ckps + pc - 1) * GS + q) * J + ln.job];
+  const int S0 = UCFG ? a.cfg_stages[c0] : 0;
+  const bool on = true;
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, FULL, true>(
+      a, s, msk, ln, lane, S0, pb, pe, on, [](int64_t) { return 2; },
+      [&](int64_t i, int r, double out, bool sv, bool rows) {
+        (void)r;
+        (void)sv;
+        if (rows && ln.valid) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
+      },
+      [](int64_t, int) {});
 }
 
 // Round q >= 1: a segment whose start state differs from its predecessor's
@@ -737,7 +786,6 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   }
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int S0 = UCFG ? a.cfg_stages[c0] : 0;
-  const bool wave_rows = __builtin_amdgcn_ballot_w64(ln.frow >= 0) != 0;
   if (lane < JPW)
     for (int x = 0; x < GS; ++x) s.F[x * JPW + lane] = active ? E_in[prv + (size_t)x * J] : 0.0;
 
@@ -747,7 +795,7 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
   bool coupled = false, gave_up = false;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA, false, true>(
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, false, false>(
       a, s, msk, ln, lane, S0, b, e, active,
       [&](int64_t cb) {
         if (cb > b && (cb - b) % a.ck == 0 && active) {
@@ -786,12 +834,14 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
           gave_up = true;
           return 0;
         }
-        return any ? (wave_rows ? 2 : 1) : 0;
+        return any ? 1 : 0;
       },
       [&](int64_t i, int r, double out, bool sv, bool rows) {
+        (void)i;
+        (void)r;
+        (void)rows;
         fsum += sv ? bits_of(out) : 0;
         word = push_bit(word, sv);
-        if (rows && ln.frow >= 0 && active) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [&](int64_t cb, int cnt) {
         word = chunk_word(word, cnt);
@@ -900,11 +950,6 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
   }
   const double dl_lane = lane < a.M ? a.d_single[lane] : 1.0;
   __syncthreads();
-  int frow = -1;
-  if (valid)
-    for (int f = 0; f < a.n_finish; ++f)
-      if (a.finish_jobs[f] == job) frow = f;
-  const bool wave_rows = __builtin_amdgcn_ballot_w64(frow >= 0) != 0;
   double F[SMAX];
 #pragma unroll
   for (int st = 0; st < SMAX; ++st) F[st] = (mine && active) ? E_in[prv + (size_t)st * J] : 0.0;
@@ -1010,16 +1055,6 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
         fsum += bits_of(prev);
       }
       if ((__builtin_amdgcn_ballot_w64(acc) & field) != 0) word |= 1ull << r;
-      if (wave_rows) {
-        const bool any_host = (__builtin_amdgcn_ballot_w64(host) & field) != 0;
-        if (frow >= 0) {
-          if (chosen) {
-            a.out_finish[(int64_t)frow * a.n + cb + r] = acc ? prev : -1.0;
-          } else if (g == 0 && !any_host) {
-            a.out_finish[(int64_t)frow * a.n + cb + r] = -2.0;
-          }
-        }
-      }
     }
     if (active && g == 0) a.bitmap[(cb >> 6) * J + job] = word;
   }
@@ -1184,6 +1219,19 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
       hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW, false>), grid, block, lds_g, s, a, q);
       hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW, true>), grid, block, lds_g, s, a, q);
     }
+  }
+  if (a.n_finish > 0) {
+    // the output rows, from the exact saved states, all pieces at once
+    const dim3 rgrid((unsigned)((int64_t)((a.n_finish + JPW - 1) / JPW) * a.nseg * (a.ckps + 1)));
+    if (spec_full<SMAX>(a)) {
+      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, false, true>), rgrid, block, lds_u, s, a);
+      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, true, true>), rgrid, block, lds_u, s, a);
+    } else {
+      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, false, false>), rgrid, block, lds_u, s, a);
+      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, true, false>), rgrid, block, lds_u, s, a);
+    }
+    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW, false, false>), rgrid, block, lds_g, s, a);
+    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW, true, false>), rgrid, block, lds_g, s, a);
   }
   hipLaunchKernelGGL(spec_final, dim3((unsigned)((a.J + 63) / 64)), block, 0, s, a);
   return hipGetLastError();
