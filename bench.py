@@ -60,19 +60,19 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "18f1a94944a2b739fb15cf38b2485210e3c095539eda4de69f6e3cd45694e7e4",
+    "sources_sha256": "6ddbcbe6f4ad4d850e1e5a8a3b922fd722672f117f8158abb8b0843a3c35ce4a",
     # one step of the heavy-trace workload runs the segment-speculative
-    # pipeline (configuration check, pass 0, reconciliation rounds, digest):
-    # its counters summed over the step's dispatches
-    "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_final + spec_cfg_check "
-              "(+ the pass-0 variants that return at once)",
-    "fetch_kib": 2160561.94, "write_kib": 5990875.75,
+    # pipeline (configuration check, pass 0, reconciliation rounds, output
+    # rows, digest): its counters summed over the step's dispatches
+    "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_rows<4, 32, true, 64, true, true> "
+              "+ spec_final + spec_cfg_check (+ the variants that return at once)",
+    "fetch_kib": 2210222.25, "write_kib": 5990700.81,
     "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "18f1a94944a2b739fb15cf38b2485210e3c095539eda4de69f6e3cd45694e7e4",
+    "sources_sha256": "6ddbcbe6f4ad4d850e1e5a8a3b922fd722672f117f8158abb8b0843a3c35ce4a",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595574.44, "write_kib": 14016.72,
+    "fetch_kib": 2595571.69, "write_kib": 14014.56,
     "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
 }
 
