@@ -691,6 +691,46 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL>(a, lds, lane, k, ln, c0);
 }
 
+// Per job: served counts and finish-time sums over the segments, and the
+// ordered hash over the accept words (the final step of the pipeline).
+__device__ __forceinline__ void final_body(const SpecArgs& a, int64_t job) {
+  if (job >= a.J) return;
+  const int64_t J = a.J;
+  int64_t served = 0;
+  uint64_t fsum = 0;
+  for (int k = 0; k < a.nseg; ++k) {
+    served += a.seg_served[(size_t)k * J + job];
+    fsum += a.seg_fsum[(size_t)k * J + job];
+  }
+  // the hash is sequential over words: the next 16 words are loaded while
+  // the current 16 are folded in
+  constexpr int kB = 16;
+  uint64_t h = 0;
+  const uint64_t* col = a.bitmap + job;
+  const int64_t nb = a.nw / kB;
+  uint64_t cur[kB], nxt[kB];
+  if (nb > 0) {
+#pragma unroll
+    for (int q = 0; q < kB; ++q) cur[q] = col[(int64_t)q * J];
+  }
+  for (int64_t bi = 0; bi < nb; ++bi) {
+    const int64_t nbase = (bi + 1 < nb ? bi + 1 : bi) * kB;
+#pragma unroll
+    for (int q = 0; q < kB; ++q) nxt[q] = col[(nbase + q) * J];
+#pragma unroll
+    for (int q = 0; q < kB; ++q) h = (h ^ cur[q]) * kSpecHashMul;
+#pragma unroll
+    for (int q = 0; q < kB; ++q) cur[q] = nxt[q];
+  }
+  for (int64_t w = nb * kB; w < a.nw; ++w) h = (h ^ col[w * J]) * kSpecHashMul;
+  a.out_served[job] = served;
+  if (a.out_attain) a.out_attain[job] = a.n > 0 ? (double)served / (double)a.n : 0.0;
+  if (a.out_digest) {
+    a.out_digest[2 * job] = h;
+    a.out_digest[2 * job + 1] = fsum;
+  }
+}
+
 // Per-request output rows of the jobs that have one.  Pass 0 and the rounds
 // write none: once the rounds are done, every saved state is the exact state
 // at its point of the trace (a segment's start, and every ck requests into
@@ -698,34 +738,14 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
 // it, all pieces at once, and only the rows are written.  Lanes are jobs with
 // a row (JPW per wavefront); blocks are row blocks x segments x pieces, and a
 // piece past its segment's end returns at once.
+// The extra-host code (some lane hosts a model on more than two groups) is
+// chosen per wavefront at run time, so that every row piece, and the final
+// step in the dispatch's first nfb workgroups, run in one dispatch.
 template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
-__global__ __launch_bounds__(64) void spec_rows(const SpecArgs a) {
-  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels write the rows
-  if ((a.cfg_info[0] != 0) != UCFG) return;
-  const int c0 = UCFG ? a.cfg_info[1] : 0;
-  extern __shared__ double lds[];
-  const int lane = threadIdx.x;
-  const int nrb = (a.n_finish + JPW - 1) / JPW;
-  const int np = a.ckps + 1;
-  const int rb = blockIdx.x % nrb;
-  const int pc = (blockIdx.x / nrb) % np;
-  const int k = blockIdx.x / (nrb * np);
-  const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
-  const int64_t pb = b + (int64_t)pc * a.ck;
-  if (pb >= e) return;
-  const int64_t pe = e - pb < a.ck ? e : pb + a.ck;
-  SpecLane ln;
-  const int f = rb * JPW + lane;
-  ln.valid = lane < JPW && f < a.n_finish;
-  ln.job = ln.valid ? a.finish_jobs[f] : 0;
-  ln.p = ln.valid ? ln.job / a.K : 0;
-  ln.scale = ln.valid ? a.slo_scale[ln.job % a.K] : 0.0;
-  ln.frow = ln.valid ? f : -1;
-  LaneMasks<MB> msk;
-  {
-    const bool many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
-    if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
-  }
+__device__ __forceinline__ void rows_body(const SpecArgs& a, double* lds, int lane, const SpecLane& ln, int c0,
+                                          int k, int pc, int64_t pb, int64_t pe) {
+  LaneMasks<MB> msk;  // loaded again here: one copy per body keeps it in registers
+  (void)msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
   const int GS = a.G * SMAX;
   const int64_t J = a.J;
@@ -744,6 +764,45 @@ __global__ __launch_bounds__(64) void spec_rows(const SpecArgs a) {
         if (rows && ln.valid) a.out_finish[(int64_t)ln.frow * a.n + i] = out;
       },
       [](int64_t, int) {});
+}
+
+template <int SMAX, int MB, bool UCFG, int JPW, bool FULL>
+__global__ __launch_bounds__(64) void spec_rows(const SpecArgs a, int nfb) {
+  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels write the rows
+  if ((a.cfg_info[0] != 0) != UCFG) return;
+  if ((int)blockIdx.x < nfb) {
+    final_body(a, (int64_t)blockIdx.x * 64 + threadIdx.x);
+    return;
+  }
+  const int bx = (int)blockIdx.x - nfb;
+  const int c0 = UCFG ? a.cfg_info[1] : 0;
+  extern __shared__ double lds[];
+  const int lane = threadIdx.x;
+  const int nrb = (a.n_finish + JPW - 1) / JPW;
+  const int np = a.ckps + 1;
+  const int rb = bx % nrb;
+  const int pc = (bx / nrb) % np;
+  const int k = bx / (nrb * np);
+  const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
+  const int64_t pb = b + (int64_t)pc * a.ck;
+  if (pb >= e) return;
+  const int64_t pe = e - pb < a.ck ? e : pb + a.ck;
+  SpecLane ln;
+  const int f = rb * JPW + lane;
+  ln.valid = lane < JPW && f < a.n_finish;
+  ln.job = ln.valid ? a.finish_jobs[f] : 0;
+  ln.p = ln.valid ? ln.job / a.K : 0;
+  ln.scale = ln.valid ? a.slo_scale[ln.job % a.K] : 0.0;
+  ln.frow = ln.valid ? f : -1;
+  bool many;
+  {
+    LaneMasks<MB> msk;
+    many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
+  }
+  if (__builtin_amdgcn_ballot_w64(many) != 0)
+    rows_body<SMAX, MB, UCFG, JPW, true, FULL>(a, lds, lane, ln, c0, k, pc, pb, pe);
+  else
+    rows_body<SMAX, MB, UCFG, JPW, false, FULL>(a, lds, lane, ln, c0, k, pc, pb, pe);
 }
 
 // Round q >= 1: a segment whose start state differs from its predecessor's
@@ -890,7 +949,10 @@ __device__ __forceinline__ uint32_t seg_min_u32w(uint32_t x) {
 // stage free times in registers and the dispatch a DPP min over the W lanes.
 // A round re-runs only a few jobs, and its time is the longest re-run: per
 // request this layout has a shorter dependency chain than one lane per job.
-template <int W, int SMAX>
+// FULL: every configuration has SMAX stages, so no stage of the chain is
+// skipped.  A lane collects the accept bits of the requests it commits; the
+// job's word is their OR over its W lanes once per chunk.
+template <int W, int SMAX, bool FULL>
 __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
   constexpr int JW = 64 / W;  // jobs per wavefront
   if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels take over
@@ -1008,8 +1070,8 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
       if (lane == 0) a.cfg_info[2] = 1;
       return;
     }
-    const int cnt = (int)(e - cb < 64 ? e - cb : 64);
-    uint64_t word = 0;
+    const int cnt = __builtin_amdgcn_readfirstlane((int)(e - cb < 64 ? e - cb : 64));
+    uint64_t lw = 0;  // accept bits of the requests this lane committed
     for (int r = 0; r < cnt; ++r) {
       const double ti = readlane_f64(tc.tv, r);
       const int m = __builtin_amdgcn_readlane(tc.mv, r);
@@ -1042,9 +1104,14 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
 #pragma unroll
       for (int st = 0; st < SMAX; ++st) {
         const double x = vmax(prev, F[st]) + L[st];
-        const bool in = st < Sg;
-        f[st] = in ? x : F[st];
-        prev = in ? x : prev;
+        if constexpr (FULL) {
+          f[st] = x;
+          prev = x;
+        } else {
+          const bool in = st < Sg;
+          f[st] = in ? x : F[st];
+          prev = in ? x : prev;
+        }
       }
       const double deadline = ti + scale * readlane_f64(dl_lane, mi);
       const bool acc = chosen && !(prev > deadline);
@@ -1053,9 +1120,10 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
         for (int st = 0; st < SMAX; ++st) F[st] = f[st];
         served += 1;
         fsum += bits_of(prev);
+        lw |= 1ull << r;
       }
-      if ((__builtin_amdgcn_ballot_w64(acc) & field) != 0) word |= 1ull << r;
     }
+    const uint64_t word = seg_or<W>(lw);  // every lane: the word of its job
     if (active && g == 0) a.bitmap[(cb >> 6) * J + job] = word;
   }
   const uint64_t js = seg_sum_u64<W>(served), jf = seg_sum_u64<W>(fsum);  // uniform flow
@@ -1091,42 +1159,7 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
 // Per job: totals over segments and the ordered digest over the accept words.
 __global__ __launch_bounds__(64) void spec_final(const SpecArgs a) {
   if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels write the results
-  const int64_t job = (int64_t)blockIdx.x * 64 + threadIdx.x;
-  if (job >= a.J) return;
-  const int64_t J = a.J;
-  int64_t served = 0;
-  uint64_t fsum = 0;
-  for (int k = 0; k < a.nseg; ++k) {
-    served += a.seg_served[(size_t)k * J + job];
-    fsum += a.seg_fsum[(size_t)k * J + job];
-  }
-  // the hash is sequential over words: the next 16 words are loaded while
-  // the current 16 are folded in
-  constexpr int kB = 16;
-  uint64_t h = 0;
-  const uint64_t* col = a.bitmap + job;
-  const int64_t nb = a.nw / kB;
-  uint64_t cur[kB], nxt[kB];
-  if (nb > 0) {
-#pragma unroll
-    for (int q = 0; q < kB; ++q) cur[q] = col[(int64_t)q * J];
-  }
-  for (int64_t bi = 0; bi < nb; ++bi) {
-    const int64_t nbase = (bi + 1 < nb ? bi + 1 : bi) * kB;
-#pragma unroll
-    for (int q = 0; q < kB; ++q) nxt[q] = col[(nbase + q) * J];
-#pragma unroll
-    for (int q = 0; q < kB; ++q) h = (h ^ cur[q]) * kSpecHashMul;
-#pragma unroll
-    for (int q = 0; q < kB; ++q) cur[q] = nxt[q];
-  }
-  for (int64_t w = nb * kB; w < a.nw; ++w) h = (h ^ col[w * J]) * kSpecHashMul;
-  a.out_served[job] = served;
-  if (a.out_attain) a.out_attain[job] = a.n > 0 ? (double)served / (double)a.n : 0.0;
-  if (a.out_digest) {
-    a.out_digest[2 * job] = h;
-    a.out_digest[2 * job + 1] = fsum;
-  }
+  final_body(a, (int64_t)blockIdx.x * 64 + threadIdx.x);
 }
 
 }  // namespace
@@ -1169,13 +1202,28 @@ __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg,
   }
 }
 
+// Whether every configuration has SMAX stages: a uniform configuration is
+// then the deepest kind, and pass 0 and the rounds run every stage of the chain.
+template <int SMAX>
+bool spec_full(const SpecArgs& a) {
+  for (int c = 0; c < a.C; ++c)
+    if (a.cfg_stages[c] != SMAX) return false;
+  return true;
+}
+
 // Rounds in the group-per-lane layout (jobs of at most 16 groups).
 template <int W, int SMAX>
 void spec_rounds_gpl(const SpecArgs& a, hipStream_t s) {
   const int njbw = (a.J + 64 / W - 1) / (64 / W);
   const dim3 grid((unsigned)((int64_t)njbw * a.nseg)), block(64);
   const size_t lds = (size_t)a.M * a.C * SMAX * 8;
-  for (int q = 1; q < a.nseg; ++q) hipLaunchKernelGGL((spec_round_gpl<W, SMAX>), grid, block, lds, s, a, q);
+  const bool full = spec_full<SMAX>(a);
+  for (int q = 1; q < a.nseg; ++q) {
+    if (full)
+      hipLaunchKernelGGL((spec_round_gpl<W, SMAX, true>), grid, block, lds, s, a, q);
+    else
+      hipLaunchKernelGGL((spec_round_gpl<W, SMAX, false>), grid, block, lds, s, a, q);
+  }
 }
 
 template <int SMAX>
@@ -1189,14 +1237,6 @@ void spec_rounds_gpl_w(const SpecArgs& a, hipStream_t s) {
   }
 }
 
-// Whether every configuration has SMAX stages: a uniform configuration is
-// then the deepest kind, and pass 0 runs every stage of the chain.
-template <int SMAX>
-bool spec_full(const SpecArgs& a) {
-  for (int c = 0; c < a.C; ++c)
-    if (a.cfg_stages[c] != SMAX) return false;
-  return true;
-}
 
 template <int SMAX, int MB, int JPW>
 hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
@@ -1220,20 +1260,19 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
       hipLaunchKernelGGL((spec_round<SMAX, MB, false, JPW, true>), grid, block, lds_g, s, a, q);
     }
   }
+  const int nfb = (int)((a.J + 63) / 64);
   if (a.n_finish > 0) {
-    // the output rows, from the exact saved states, all pieces at once
-    const dim3 rgrid((unsigned)((int64_t)((a.n_finish + JPW - 1) / JPW) * a.nseg * (a.ckps + 1)));
-    if (spec_full<SMAX>(a)) {
-      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, false, true>), rgrid, block, lds_u, s, a);
-      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, true, true>), rgrid, block, lds_u, s, a);
-    } else {
-      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, false, false>), rgrid, block, lds_u, s, a);
-      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, true, false>), rgrid, block, lds_u, s, a);
-    }
-    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW, false, false>), rgrid, block, lds_g, s, a);
-    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW, true, false>), rgrid, block, lds_g, s, a);
+    // the output rows, from the exact saved states, all pieces at once, and
+    // in the same dispatch (its first nfb workgroups) the final step
+    const dim3 rgrid((unsigned)(nfb + (int64_t)((a.n_finish + JPW - 1) / JPW) * a.nseg * (a.ckps + 1)));
+    if (spec_full<SMAX>(a))
+      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, true>), rgrid, block, lds_u, s, a, nfb);
+    else
+      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, false>), rgrid, block, lds_u, s, a, nfb);
+    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW, false>), rgrid, block, lds_g, s, a, nfb);
+  } else {
+    hipLaunchKernelGGL(spec_final, dim3((unsigned)nfb), block, 0, s, a);
   }
-  hipLaunchKernelGGL(spec_final, dim3((unsigned)((a.J + 63) / 64)), block, 0, s, a);
   return hipGetLastError();
 }
 

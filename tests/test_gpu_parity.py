@@ -96,6 +96,19 @@ def test_c4_reduced_all_jobs(gpu):
     compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), len(pb.t), "c4 reduced")
 
 
+def test_c4_reduced_no_rows(gpu):
+    """The same jobs with no per-request output rows: on the speculative path
+    the digest step then runs as a dispatch of its own (with rows it shares
+    the output-row dispatch)."""
+    import dataclasses
+    from paper_2302_11665_amd.workload import problems
+    pb = problems.c4_heavy(duration=45.0, n_placements=600, n_finish=7)
+    pb = dataclasses.replace(pb, finish_jobs=np.zeros(0, np.int32))
+    say("c4 reduced, no rows", pb.n_jobs, len(pb.t))
+    res = gpu.simulate_problem(pb)
+    compare(res, oracle_problem(pb), len(pb.t), "c4 reduced no rows")
+
+
 def test_c3_candidate_steps_every_partition(gpu):
     """Greedy-step job sets of every partition of the 64-device workload:
     single-replica candidates from the empty selection, and candidates on top
