@@ -638,18 +638,39 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   st.wlo = 0;
   st.busy = 0.0;
 
+  // the segment's arrivals are requested a chunk ahead: each round stages
+  // the ones requested during the previous round, then requests the next
+  constexpr int kPer = kSegChunk / 64;  // arrivals per lane and round
+  double pt[kPer];
+  int pm[kPer];
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int64_t e = (int64_t)q * 64 + lane;
+    pt[q] = e < n_job ? a.t[begin + e] : 0.0;
+    pm[q] = e < n_job ? a.model[begin + e] : 0;
+  }
   for (int64_t base = 0; base < n_job; base += kSegChunk) {
     const int cnt = (int)((n_job - base) < kSegChunk ? (n_job - base) : kSegChunk);
     // this wavefront's chunk: the previous one has been read (in-order LDS
     // within a wavefront; the fences keep the compiler from moving accesses)
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    for (int e = lane; e < cnt; e += 64) {
-      const double te = a.t[begin + base + e];
-      const uint32_t off = (uint32_t)a.model[begin + base + e] << RSH;
-      const double de = te + *(const double*)(rec + off + rec_slo(SMAX));
-      *(double2*)(sTD + 2 * e) = make_double2(te, de);
-      sO[e] = off;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int e = q * 64 + lane;
+      if (e < cnt) {
+        const double te = pt[q];
+        const uint32_t off = (uint32_t)pm[q] << RSH;
+        const double de = te + *(const double*)(rec + off + rec_slo(SMAX));
+        *(double2*)(sTD + 2 * e) = make_double2(te, de);
+        sO[e] = off;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int64_t e = base + kSegChunk + (int64_t)q * 64 + lane;
+      pt[q] = e < n_job ? a.t[begin + e] : 0.0;
+      pm[q] = e < n_job ? a.model[begin + e] : 0;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
