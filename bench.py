@@ -60,20 +60,20 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "6ddbcbe6f4ad4d850e1e5a8a3b922fd722672f117f8158abb8b0843a3c35ce4a",
+    "sources_sha256": "8a5b4c1727bdb09be57884e0ecb0cac212f85bc3a520e1ea26bb01c060e69b58",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, output
     # rows, digest): its counters summed over the step's dispatches
-    "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4> + spec_rows<4, 32, true, 64, true, true> "
-              "+ spec_final + spec_cfg_check (+ the variants that return at once)",
-    "fetch_kib": 2210222.25, "write_kib": 5990700.81,
-    "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
+    "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_gpl<16, 4, true> + spec_rows<4, 32, true, 64, "
+              "true> (row pieces and the final step) + spec_cfg_check (+ the variants that return at once)",
+    "fetch_kib": 2207090.38, "write_kib": 5990715.56,
+    "fetch_scale": 1048576.0 / 524302.14, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "6ddbcbe6f4ad4d850e1e5a8a3b922fd722672f117f8158abb8b0843a3c35ce4a",
+    "sources_sha256": "8a5b4c1727bdb09be57884e0ecb0cac212f85bc3a520e1ea26bb01c060e69b58",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595571.69, "write_kib": 14014.56,
-    "fetch_scale": 1048576.0 / 524301.94, "write_scale": 1048576.0 / 1048576.0,
+    "fetch_kib": 2595630.44, "write_kib": 14017.25,
+    "fetch_scale": 1048576.0 / 524302.14, "write_scale": 1048576.0 / 1048576.0,
 }
 
 
