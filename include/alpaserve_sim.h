@@ -156,9 +156,12 @@ typedef struct {
  *                    finish_jobs[f]'s outputs for requests i < min(segment
  *                    length, finish_stride)
  * Asynchronous on `stream`.  With more than 32 groups (one job per
- * wavefront) and 2..4096 jobs, the jobs are launched longest and shortest
- * segment alternating, which changes no result; the order array (4 bytes
- * per job) comes from the library's memory pool and is released
+ * wavefront at a time) and 2..4096 jobs, the jobs are sorted by segment
+ * length on the device: up to two wavefronts per SIMD they run one per
+ * wavefront, longest and shortest segment alternating; beyond, two
+ * wavefronts per SIMD take them in turn, longest first, from a counter.
+ * Neither changes any result.  The order array and the counter (4 bytes per
+ * job, plus 4) come from the library's memory pool and are released
  * stream-ordered.
  */
 int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_offsets,

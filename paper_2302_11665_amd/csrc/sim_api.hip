@@ -569,11 +569,14 @@ namespace {
 constexpr int kOrderMaxJobs = 4096;  // jobs the one-workgroup sort below takes
 
 // Launch order of the one-job-per-wavefront kernel: the jobs sorted by
-// segment length (longest first, lower index first on ties), then the
-// longest and the shortest alternating -- order[2i] the i-th longest,
-// order[2i + 1] the i-th shortest -- so that the longest chains share their
-// SIMDs with short ones.  One workgroup of 1024 threads, J <= 4096.
-__global__ __launch_bounds__(1024) void seg_order(const KArgs a, int32_t* __restrict__ order) {
+// segment length (longest first, lower index first on ties).  queue 0: one
+// job per wavefront, the longest and the shortest alternating -- order[2i]
+// the i-th longest, order[2i + 1] the i-th shortest -- so that the longest
+// chains share their SIMDs with short ones.  queue 1: fewer wavefronts than
+// jobs take the jobs in turn, longest first, from the slot counter
+// order[J], which is set to 0 here.  One workgroup of 1024 threads,
+// J <= 4096.
+__global__ __launch_bounds__(1024) void seg_order(const KArgs a, int32_t* __restrict__ order, int queue) {
   __shared__ int64_t key[kOrderMaxJobs];
   __shared__ int32_t val[kOrderMaxJobs];
   const int J = (int)a.J;
@@ -619,8 +622,28 @@ __global__ __launch_bounds__(1024) void seg_order(const KArgs a, int32_t* __rest
   }
   for (int i = threadIdx.x; i < J; i += blockDim.x) {
     const int h = i >> 1;
-    order[i] = (i & 1) == 0 ? val[h] : val[J - 1 - h];
+    order[i] = queue ? val[i] : (i & 1) == 0 ? val[h] : val[J - 1 - h];
   }
+  if (queue && threadIdx.x == 0) order[J] = 0;
+}
+
+// Wavefronts per SIMD that take the sweep's jobs in turn.  Two: the longest
+// job shares its SIMD with one other wavefront, which works through shorter
+// jobs meanwhile (ALPASERVE_SEG_WAVES sets 1-4, for measurements).
+int seg_waves_per_simd() {
+  const char* e = getenv("ALPASERVE_SEG_WAVES");
+  const int v = e ? atoi(e) : 2;
+  return v < 1 ? 1 : (v > 4 ? 4 : v);
+}
+
+// Workgroups that take the jobs in turn: seg_waves_per_simd() per compute
+// unit (ALPASERVE_SEG_BLOCKS sets the count, 1-4096, for the tests: a few
+// workgroups then each work through many jobs).
+int64_t seg_queue_blocks(int wps) {
+  const char* e = getenv("ALPASERVE_SEG_BLOCKS");
+  const int v = e ? atoi(e) : 0;
+  if (v >= 1 && v <= 4096) return v;
+  return (int64_t)wps * as_host::compute_units();
 }
 
 }  // namespace
@@ -669,21 +692,37 @@ int as_simulate_jobs(const double* t, const int32_t* model, const int64_t* seg_o
       if ((e = hipGetLastError()) != hipSuccess)
         return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     }
-    // long and short chains interleaved (skipped, never an error, where the
-    // jobs are too many for the sort or its array cannot be allocated)
+    // Jobs longest first.  With more jobs than seg_waves_per_simd()
+    // wavefronts per SIMD, that many wavefronts take them in turn (each
+    // compute unit holds that many workgroups of one wavefront per SIMD: the
+    // LDS request leaves room for no more); otherwise one job per wavefront,
+    // long and short chains interleaved.  Skipped, never an error, where the
+    // jobs are too many for the sort or its array cannot be allocated.
+    const int wps = as_dev::seg_waves_per_simd();
+    const int64_t queue_blocks = as_dev::seg_queue_blocks(wps);
+    int64_t blocks = (n_jobs + as_dev::kWaves - 1) / as_dev::kWaves;
+    size_t lds = lds_seg;
     int32_t* order = nullptr;
     if (n_jobs >= 2 && n_jobs <= as_dev::kOrderMaxJobs &&
-        pool_alloc(reinterpret_cast<void**>(&order), (size_t)n_jobs * 4, s) == hipSuccess) {
-      hipLaunchKernelGGL(as_dev::seg_order, dim3(1), dim3(1024), 0, s, a, order);
+        pool_alloc(reinterpret_cast<void**>(&order), ((size_t)n_jobs + 1) * 4, s) == hipSuccess) {
+      const bool queue = blocks > queue_blocks;
+      hipLaunchKernelGGL(as_dev::seg_order, dim3(1), dim3(1024), 0, s, a, order, queue ? 1 : 0);
       if ((e = hipGetLastError()) != hipSuccess) {
         (void)hipFreeAsync(order, s);
         return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
       }
       a.order = order;
+      if (queue) {
+        a.next_slot = order + n_jobs;
+        blocks = queue_blocks;
+        const size_t per_cu = 160 * 1024;  // LDS of a compute unit
+        const size_t cap = per_cu / (size_t)(wps + 1) + 1024;
+        if (cap > lds && cap <= shared_lds_limit()) lds = cap;
+      }
     } else {
       (void)hipGetLastError();
     }
-    e = as_host::launch_seg64(smax, a, lds_seg, s);
+    e = as_host::launch_seg64(smax, a, blocks, lds, s);
     const hipError_t ef = order ? hipFreeAsync(order, s) : hipSuccess;
     if (e != hipSuccess) return fail(AS_E_HIP, "kernel launch failed: %s", hipGetErrorString(e));
     if (ef != hipSuccess) return fail(AS_E_HIP, "order release failed: %s", hipGetErrorString(ef));

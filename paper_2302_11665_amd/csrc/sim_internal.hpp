@@ -20,6 +20,8 @@ int ok();
 int pow2ceil(int x);
 // LDS a workgroup may use on the current device (160 KiB on gfx950).
 size_t shared_lds_limit();
+// Compute units of the current device (cached per device).
+int compute_units();
 // Stream-ordered device allocation from the library's private memory pool
 // (one per device, memory kept for reuse between calls); release with
 // hipFreeAsync on a stream ordered after the last use.

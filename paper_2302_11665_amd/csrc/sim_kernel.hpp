@@ -61,6 +61,8 @@ struct KArgs {
   const int64_t* seg_off;  // segmented: [n_segments + 1]
   const as_job_t* jobs;    // segmented: [J]
   const int32_t* order;    // segmented, one job per wavefront: slot -> job, a permutation (null: identity)
+  int32_t* next_slot;      // segmented: set, the wavefronts take slots in turn from this counter (0 at
+                           // launch) until all are taken; null: wavefront w runs slot w
   const double* d_single;
   const double* stage_lat;
   const int32_t* group_cfg;

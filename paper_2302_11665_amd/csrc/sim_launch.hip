@@ -73,8 +73,8 @@ hipError_t launch_shared(int smax, bool usig, bool stats, const KArgs& a, size_t
 }
 
 #if AS_W == 64
-hipError_t launch_seg64(int smax, const KArgs& a, size_t lds, hipStream_t s) {
-  const int grid = (a.J + as_dev::kWaves - 1) / as_dev::kWaves;
+hipError_t launch_seg64(int smax, const KArgs& a, int64_t blocks, size_t lds, hipStream_t s) {
+  const unsigned grid = (unsigned)blocks;
   switch (smax) {
     case 1:
       hipLaunchKernelGGL((as_dev::seg_kernel<1>), dim3(grid), dim3(as_dev::kThreads), lds, s, a);

@@ -26,9 +26,11 @@ hipError_t launch_shared(int smax, bool usig, bool stats, const KArgs& a, size_t
 hipError_t launch_shared_multi(bool stats, const KArgs* a_dev, const as_dev::MultiSegs& ms, int64_t blocks,
                                size_t lds, hipStream_t s);
 
-// Segmented jobs with up to 64 groups, one job per wavefront (built in the
-// 64-lane unit).
-hipError_t launch_seg64(int smax, const KArgs& a, size_t lds, hipStream_t s);
+// Segmented jobs with up to 64 groups, one job per wavefront at a time
+// (built in the 64-lane unit): blocks workgroups of kWaves wavefronts, each
+// wavefront running slot blockIdx * kWaves + w, or taking slots in turn
+// from a.next_slot when that is set.
+hipError_t launch_seg64(int smax, const KArgs& a, int64_t blocks, size_t lds, hipStream_t s);
 
 #define AS_DECLARE_W(W)                                                                       \
   extern template hipError_t launch_lds<W>(int, int, bool, const KArgs&, size_t, hipStream_t); \

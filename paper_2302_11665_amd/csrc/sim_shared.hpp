@@ -539,8 +539,11 @@ __device__ __forceinline__ void seg_job(const KArgs& a, int64_t j, int& p, doubl
 }
 
 // Slot blockIdx.x * kWaves + wavefront runs job order[slot] (the slot itself
-// without an order).  Per-request output rows must hold -2 over
-// [0, min(segment length, finish_stride)) when the kernel starts.
+// without an order); with a slot counter (a.next_slot, 0 at launch) each
+// wavefront instead takes slots in turn until none is left, so that a grid
+// of fewer wavefronts than jobs works through a longest-first order.
+// Per-request output rows must hold -2 over [0, min(segment length,
+// finish_stride)) when the kernel starts.
 template <int SMAX>
 __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   constexpr int W = 64;
@@ -557,49 +560,12 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int64_t slot = (int64_t)blockIdx.x * kWaves + wave;
-  const bool job_ok = slot < a.J;
-  const int64_t job = job_ok && a.order ? (int64_t)a.order[slot] : slot;
   double* sTD = sTDall + (size_t)wave * 2 * kSegChunk;
   uint32_t* sO = sOall + (size_t)wave * kSegChunk;
-
-  int p = 0;
-  double sigma = 0.0;
-  int64_t begin = 0, n_job = 0;
-  if (job_ok) seg_job(a, job, p, sigma, begin, n_job);
-
-  SharedConst c;
-  c.sigma = sigma;
-  int cfg = -1;
-  if (job_ok && lane < a.G) cfg = a.group_cfg[(int64_t)p * a.G + lane];
-  if (cfg >= a.C || cfg < 0) cfg = -1;
-  uint64_t hostbits = 0;  // bit m: this lane's group hosts model m
-  if (cfg >= 0) {
-    const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
-    for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> lane) & 1u) << m;
-  }
-  int frow = -1;
-  if (job_ok)
-    for (int f = 0; f < a.n_finish; ++f)
-      if (a.finish_jobs[f] == job) {
-        frow = f;
-        break;
-      }
-  c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
-  c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.finish_stride);
-  c.flimit = n_job < a.finish_stride ? n_job : a.finish_stride;
-  const bool wave_finish = c.fmask != 0;
-  // whether the row is shorter than the segment (else no per-request limit test)
-  const bool row_lim = c.flimit < n_job;
-  if (wave_finish) __builtin_amdgcn_s_setprio(3);
-  const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
-  const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
-  const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
-  c.lrow = sL + (cfg < 0 ? 0 : cfg) * SMAX;
-  c.lshift = lshift;
   unsigned char* rec = sR + (size_t)wave * a.M * (1 << RSH);
-  c.rec = rec;
 
+  // the stage-latency table, once per workgroup (the only barrier: after it
+  // every wavefront goes its own way)
   const int nL = a.M * cp * SMAX;
   for (int idx = tid; idx < nL; idx += kThreads) {
     const int s = idx % SMAX;
@@ -610,96 +576,153 @@ __global__ __launch_bounds__(kThreads) void seg_kernel(const KArgs a) {
                   ? a.stage_lat[((int64_t)m * a.C + cc) * a.smax_in + s]
                   : 0.0;
   }
-  for (int m = 0; m < a.M; ++m) {
-    const uint64_t hm = __builtin_amdgcn_ballot_w64((hostbits >> m) & 1u);
-    if (lane == 0) {
-      const uint64_t one = lowest_per_field<W>(hm);
-      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecMask) = hm;
-      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount) =
-          one == hm ? 0u : (uint32_t)__builtin_popcountll(one);
-    }
-  }
-  for (int m = lane; m < a.M; m += 64) {
-    unsigned char* r = rec + ((size_t)m << RSH);
-    // this job's SLO of model m: scale * d_single[m] (one rounding)
-    *(double*)(r + rec_slo(SMAX)) = sigma * a.d_single[m];
-#pragma unroll
-    for (int s = 0; s < SMAX; ++s)
-      ((double*)(r + kRecLat))[s] = (uni && s < a.cfg_stages[cfg0])
-                                        ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + s]
-                                        : 0.0;
-  }
   __syncthreads();
 
-  SharedLane<SMAX> st;
-#pragma unroll
-  for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
-  st.fin_sum = st.hash = st.served = 0;
-  st.wlo = 0;
-  st.busy = 0.0;
+  auto take_slot = [&]() -> int64_t {
+    int v = 0;
+    if (lane == 0) v = atomicAdd(a.next_slot, 1);
+    return (int64_t)__builtin_amdgcn_readfirstlane(v);
+  };
+  int64_t slot = a.next_slot ? take_slot() : (int64_t)blockIdx.x * kWaves + wave;
+  while (slot < a.J) {
+    const int64_t job = a.order ? (int64_t)a.order[slot] : slot;
+    int p = 0;
+    double sigma = 0.0;
+    int64_t begin = 0, n_job = 0;
+    seg_job(a, job, p, sigma, begin, n_job);
 
-  // the segment's arrivals are requested a chunk ahead: each round stages
-  // the ones requested during the previous round, then requests the next
-  constexpr int kPer = kSegChunk / 64;  // arrivals per lane and round
-  double pt[kPer];
-  int pm[kPer];
-#pragma unroll
-  for (int q = 0; q < kPer; ++q) {
-    const int64_t e = (int64_t)q * 64 + lane;
-    pt[q] = e < n_job ? a.t[begin + e] : 0.0;
-    pm[q] = e < n_job ? a.model[begin + e] : 0;
-  }
-  for (int64_t base = 0; base < n_job; base += kSegChunk) {
-    const int cnt = (int)((n_job - base) < kSegChunk ? (n_job - base) : kSegChunk);
-    // this wavefront's chunk: the previous one has been read (in-order LDS
-    // within a wavefront; the fences keep the compiler from moving accesses)
+    SharedConst c;
+    c.sigma = sigma;
+    int cfg = -1;
+    if (lane < a.G) cfg = a.group_cfg[(int64_t)p * a.G + lane];
+    if (cfg >= a.C || cfg < 0) cfg = -1;
+    uint64_t hostbits = 0;  // bit m: this lane's group hosts model m
+    if (cfg >= 0) {
+      const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
+      for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> lane) & 1u) << m;
+    }
+    int frow = -1;
+    for (int f = 0; f < a.n_finish; ++f)
+      if (a.finish_jobs[f] == job) {
+        frow = f;
+        break;
+      }
+    c.fmask = __builtin_amdgcn_ballot_w64(frow >= 0);
+    c.frowp = a.out_finish + (frow < 0 ? 0 : (int64_t)frow * a.finish_stride);
+    c.flimit = n_job < a.finish_stride ? n_job : a.finish_stride;
+    const bool wave_finish = c.fmask != 0;
+    // whether the row is shorter than the segment (else no per-request limit test)
+    const bool row_lim = c.flimit < n_job;
+    if (wave_finish)
+      __builtin_amdgcn_s_setprio(3);
+    else
+      __builtin_amdgcn_s_setprio(0);
+    const uint64_t valid = __builtin_amdgcn_ballot_w64(cfg >= 0);
+    const int cfg0 = valid ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(valid)) : 0;
+    const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
+    c.lrow = sL + (cfg < 0 ? 0 : cfg) * SMAX;
+    c.lshift = lshift;
+    c.rec = rec;
+
+    // this job's records: the previous job's reads of them are done (in-order
+    // LDS within a wavefront; the fences keep the compiler from moving accesses)
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int e = q * 64 + lane;
-      if (e < cnt) {
-        const double te = pt[q];
-        const uint32_t off = (uint32_t)pm[q] << RSH;
-        const double de = te + *(const double*)(rec + off + rec_slo(SMAX));
-        *(double2*)(sTD + 2 * e) = make_double2(te, de);
-        sO[e] = off;
+    for (int m = 0; m < a.M; ++m) {
+      const uint64_t hm = __builtin_amdgcn_ballot_w64((hostbits >> m) & 1u);
+      if (lane == 0) {
+        const uint64_t one = lowest_per_field<W>(hm);
+        *(uint64_t*)(rec + ((size_t)m << RSH) + kRecMask) = hm;
+        *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount) =
+            one == hm ? 0u : (uint32_t)__builtin_popcountll(one);
       }
     }
+    for (int m = lane; m < a.M; m += 64) {
+      unsigned char* r = rec + ((size_t)m << RSH);
+      // this job's SLO of model m: scale * d_single[m] (one rounding)
+      *(double*)(r + rec_slo(SMAX)) = sigma * a.d_single[m];
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int64_t e = base + kSegChunk + (int64_t)q * 64 + lane;
-      pt[q] = e < n_job ? a.t[begin + e] : 0.0;
-      pm[q] = e < n_job ? a.model[begin + e] : 0;
+      for (int s = 0; s < SMAX; ++s)
+        ((double*)(r + kRecLat))[s] = (uni && s < a.cfg_stages[cfg0])
+                                          ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + s]
+                                          : 0.0;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (uni) {
-      if (wave_finish && row_lim)
-        fast_chunk<W, SMAX, true, true, true, true>(st, c, sTD, sO, cnt, base, n_job);
-      else if (wave_finish)
-        fast_chunk<W, SMAX, true, true, false, true>(st, c, sTD, sO, cnt, base, n_job);
-      else
-        fast_chunk<W, SMAX, true, false, false, true>(st, c, sTD, sO, cnt, base, n_job);
-    } else {
-      if (wave_finish && row_lim)
-        fast_chunk<W, SMAX, true, true, true, false>(st, c, sTD, sO, cnt, base, n_job);
-      else if (wave_finish)
-        fast_chunk<W, SMAX, true, true, false, false>(st, c, sTD, sO, cnt, base, n_job);
-      else
-        fast_chunk<W, SMAX, true, false, false, false>(st, c, sTD, sO, cnt, base, n_job);
-    }
-  }
 
-  const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum);
-  if (job_ok && lane == 0) {
-    a.out_served[job] = (int64_t)st.served;
-    if (a.out_attain) a.out_attain[job] = n_job > 0 ? (double)st.served / (double)n_job : 0.0;
-    if (a.out_digest) {
-      a.out_digest[2 * job] = st.hash;
-      a.out_digest[2 * job + 1] = fin_sum;
+    SharedLane<SMAX> st;
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) st.F[s] = 0.0;
+    st.fin_sum = st.hash = st.served = 0;
+    st.wlo = 0;
+    st.busy = 0.0;
+
+    // the segment's arrivals are requested a chunk ahead: each round stages
+    // the ones requested during the previous round, then requests the next
+    constexpr int kPer = kSegChunk / 64;  // arrivals per lane and round
+    double pt[kPer];
+    int pm[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int64_t e = (int64_t)q * 64 + lane;
+      pt[q] = e < n_job ? a.t[begin + e] : 0.0;
+      pm[q] = e < n_job ? a.model[begin + e] : 0;
     }
+    for (int64_t base = 0; base < n_job; base += kSegChunk) {
+      const int cnt = (int)((n_job - base) < kSegChunk ? (n_job - base) : kSegChunk);
+      // this wavefront's chunk: the previous one has been read (in-order LDS
+      // within a wavefront; the fences keep the compiler from moving accesses)
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int e = q * 64 + lane;
+        if (e < cnt) {
+          const double te = pt[q];
+          const uint32_t off = (uint32_t)pm[q] << RSH;
+          const double de = te + *(const double*)(rec + off + rec_slo(SMAX));
+          *(double2*)(sTD + 2 * e) = make_double2(te, de);
+          sO[e] = off;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int64_t e = base + kSegChunk + (int64_t)q * 64 + lane;
+        pt[q] = e < n_job ? a.t[begin + e] : 0.0;
+        pm[q] = e < n_job ? a.model[begin + e] : 0;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if (uni) {
+        if (wave_finish && row_lim)
+          fast_chunk<W, SMAX, true, true, true, true>(st, c, sTD, sO, cnt, base, n_job);
+        else if (wave_finish)
+          fast_chunk<W, SMAX, true, true, false, true>(st, c, sTD, sO, cnt, base, n_job);
+        else
+          fast_chunk<W, SMAX, true, false, false, true>(st, c, sTD, sO, cnt, base, n_job);
+      } else {
+        if (wave_finish && row_lim)
+          fast_chunk<W, SMAX, true, true, true, false>(st, c, sTD, sO, cnt, base, n_job);
+        else if (wave_finish)
+          fast_chunk<W, SMAX, true, true, false, false>(st, c, sTD, sO, cnt, base, n_job);
+        else
+          fast_chunk<W, SMAX, true, false, false, false>(st, c, sTD, sO, cnt, base, n_job);
+      }
+    }
+
+    const uint64_t fin_sum = seg_sum_u64<W>(st.fin_sum);
+    if (lane == 0) {
+      a.out_served[job] = (int64_t)st.served;
+      if (a.out_attain) a.out_attain[job] = n_job > 0 ? (double)st.served / (double)n_job : 0.0;
+      if (a.out_digest) {
+        a.out_digest[2 * job] = st.hash;
+        a.out_digest[2 * job + 1] = fin_sum;
+      }
+    }
+    if (!a.next_slot) break;
+    slot = take_slot();
   }
 }
 

@@ -1302,8 +1302,6 @@ hipError_t spec_launch_mb(int G, const SpecArgs& a, size_t l1, size_t l2, hipStr
 
 namespace as_host {
 
-namespace {
-
 int compute_units() {
   static int cache[64] = {0};
   int dev = 0;
@@ -1315,6 +1313,9 @@ int compute_units() {
   }
   return cache[dev];
 }
+
+namespace {
+
 
 
 // warm-up requests before a segment (measured on the 8192-placement workload:

@@ -157,3 +157,34 @@ def test_launch_order_does_not_change_results(dev, J):
     sample = sorted(set(rng.choice(J, size=min(J, 24), replace=False).tolist()))
     sub = dict(c, jp=c["jp"][sample], js=c["js"][sample], jsc=c["jsc"][sample])
     _check(sub, tuple(np.asarray(x)[sample] for x in ref[:3]) + (None,), [], 0)
+
+
+@pytest.mark.parametrize("J,blocks", [(13, 3), (300, 1), (1000, 3), (4096, 7)])
+def test_job_queue_matches_one_job_per_wavefront(dev, monkeypatch, J, blocks):
+    """With more jobs than the wavefronts launched, the wavefronts take the
+    jobs in turn, longest segment first, from a counter (ALPASERVE_SEG_BLOCKS
+    forces that with a few workgroups, so that each wavefront runs many jobs
+    one after the other in its own LDS records): every output, output rows
+    included, equals the one-job-per-wavefront launch's, and a sample equals
+    the oracle's."""
+    rng = np.random.default_rng(1300 + J)
+    c = _case(rng, 64, 4)
+    n_seg = len(c["offs"]) - 1
+    c = dict(c, jp=rng.integers(0, c["gcfg"].shape[0], J).astype(np.int32),
+             js=rng.integers(0, n_seg, J).astype(np.int32), jsc=rng.choice([0.5, 2.0, 5.0, np.inf], J))
+    finish = sorted(set(rng.choice(J, size=min(J, 5), replace=False).tolist()))
+    stride = 2000
+    monkeypatch.delenv("ALPASERVE_SEG_BLOCKS", raising=False)
+    monkeypatch.setenv("ALPASERVE_SEG_WAVES", "4")  # one job per wavefront for up to 4096 jobs on 256 CUs
+    say("job queue reference", J, "jobs")
+    ref = _run(dev, c, finish, stride)
+    monkeypatch.setenv("ALPASERVE_SEG_BLOCKS", str(blocks))
+    say("job queue", J, "jobs,", blocks, "workgroups")
+    got = _run(dev, c, finish, stride)
+    for a, b in zip(ref[:3], got[:3]):
+        assert np.array_equal(np.asarray(a), np.asarray(b))
+    assert ref[3].tobytes() == got[3].tobytes()
+    sample = sorted(set(rng.choice(J, size=min(J, 16), replace=False).tolist()) | set(finish))
+    sub = dict(c, jp=c["jp"][sample], js=c["js"][sample], jsc=c["jsc"][sample])
+    fin_sub = [sample.index(j) for j in finish]
+    _check(sub, tuple(np.asarray(x)[sample] for x in got[:3]) + (got[3],), fin_sub, stride)
