@@ -56,6 +56,7 @@
 #include "alpaserve_sim.h"
 #include "sim_internal.hpp"
 #include "sim_kernel.hpp"
+#include "sim_shared.hpp"
 
 namespace as_dev {
 namespace {
@@ -949,10 +950,11 @@ __device__ __forceinline__ uint32_t seg_min_u32w(uint32_t x) {
 // stage free times in registers and the dispatch a DPP min over the W lanes.
 // A round re-runs only a few jobs, and its time is the longest re-run: per
 // request this layout has a shorter dependency chain than one lane per job.
-// FULL: every configuration has SMAX stages, so no stage of the chain is
-// skipped.  A lane collects the accept bits of the requests it commits; the
-// job's word is their OR over its W lanes once per chunk.
-template <int W, int SMAX, bool FULL>
+// This kernel serves placements with configurations of fewer than SMAX
+// stages (a stage past a group's depth keeps its free time, as in pass 0);
+// spec_round_fast the rest.  A lane collects the accept bits of the requests
+// it commits; the job's word is their OR over its W lanes once per chunk.
+template <int W, int SMAX>
 __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
   constexpr int JW = 64 / W;  // jobs per wavefront
   if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels take over
@@ -1104,14 +1106,9 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
 #pragma unroll
       for (int st = 0; st < SMAX; ++st) {
         const double x = vmax(prev, F[st]) + L[st];
-        if constexpr (FULL) {
-          f[st] = x;
-          prev = x;
-        } else {
-          const bool in = st < Sg;
-          f[st] = in ? x : F[st];
-          prev = in ? x : prev;
-        }
+        const bool in = st < Sg;
+        f[st] = in ? x : F[st];
+        prev = in ? x : prev;
       }
       const double deadline = ti + scale * readlane_f64(dl_lane, mi);
       const bool acc = chosen && !(prev > deadline);
@@ -1154,6 +1151,240 @@ __global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
   if (mine)
 #pragma unroll
     for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = E_in[own + (size_t)st * J];
+}
+
+// One 64-request chunk (cnt <= 64 of them, staged in LDS) of a round in the
+// group-per-lane layout, run by the shared-trace kernel's request step;
+// returns the job's accept word (request r at bit r, in every lane of the
+// job) and adds its population count to the job's served count.
+template <int W, int SMAX, bool UNI>
+__device__ __forceinline__ uint64_t round_chunk(SharedLane<SMAX>& st, const SharedConst& c, const double* sT,
+                                                const uint32_t* sO, int cnt) {
+  uint64_t word = 0;
+  for (int h = 0; h < cnt; h += 32) {
+    const int hc = (cnt - h) < 32 ? (cnt - h) : 32;
+    uint32_t sr = 0;  // request e of the half at bit hc - 1 - e
+    if (hc == 32) {
+      for (int e = 0; e < 32; e += 4)
+        fast_batch<W, SMAX, 4, false, false, false, UNI>(st, c, sT + 2 * (h + e), sO + h + e, h + e, sr);
+    } else {
+      for (int e = 0; e < hc; ++e)
+        fast_batch<W, SMAX, 1, false, false, false, UNI>(st, c, sT + 2 * (h + e), sO + h + e, h + e, sr);
+    }
+    const uint32_t bits = hc == 32 ? __builtin_bitreverse32(sr) : (__builtin_bitreverse32(sr) >> (32 - hc));
+    word |= (uint64_t)bits << h;
+  }
+  const uint64_t wj = seg_or<W>(word);
+  st.served += (uint64_t)__popcll(wj);
+  return wj;
+}
+
+// LDS bytes of spec_round_fast: M + 1 model records (the last hosts nothing
+// and stands for an out-of-range model id), the stage-latency table
+// [M][Cp][SMAX] and one staged chunk (arrivals at stride 2, record offsets).
+__host__ __device__ constexpr size_t round_fast_lds_bytes(int M, int Cp, int SMAX) {
+  return (size_t)(M + 1) * ((size_t)1 << rec_shift(SMAX)) + (size_t)M * Cp * SMAX * 8 + 128 * 8 + 64 * 4;
+}
+
+// Round q >= 1 in the group-per-lane layout where every configuration has
+// SMAX stages: the protocol of spec_round_gpl with the shared-trace kernel's
+// request step -- per-wavefront model records in LDS (hosting lanes, the
+// count that says whether a dispatch minimum is needed, stage latencies,
+// d_single), the two-level integer minimum, four requests' inputs read
+// together -- which issues about half the instructions per request of the
+// lane-by-lane step.  Only the jobs that re-run host models in the records; a
+// job that has met the old results keeps simulating with the others but
+// writes nothing more.  Each 64-request chunk is staged in LDS from registers
+// loaded a chunk ahead.
+template <int W, int SMAX>
+__global__ __launch_bounds__(64) void spec_round_fast(const SpecArgs a, int q) {
+  constexpr int JW = 64 / W;  // jobs per wavefront
+  constexpr int RSH = rec_shift(SMAX);
+  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels take over
+  if (a.changed[q - 1] == 0) return;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const int g = lane % W, slot = lane / W;
+  const int njbw = (a.J + JW - 1) / JW;
+  const int k = blockIdx.x / njbw, jb = blockIdx.x % njbw;
+  const int job = jb * JW + slot;
+  const bool valid = job < a.J;
+  const bool mine = valid && g < a.G;  // this lane holds a group of a job
+  const int GS = a.G * SMAX;
+  const int64_t J = a.J;
+  const size_t per_buf = (size_t)a.nseg * GS * J;
+  const double* E_in = a.st_end + (size_t)((q - 1) & 1) * per_buf;
+  double* E_out = a.st_end + (size_t)(q & 1) * per_buf;
+  const size_t own = ((size_t)k * GS + (size_t)g * SMAX) * J + job;  // my group's first entry
+  const size_t prv = k > 0 ? ((size_t)(k - 1) * GS + (size_t)g * SMAX) * J + job : 0;
+  const uint64_t field = (W == 64 ? ~0ull : ((1ull << W) - 1)) << ((uint64_t)slot * W);
+
+  // stale start state?  (every lane of a job agrees through the ballot)
+  bool differ = false;
+  if (mine && k > 0)
+#pragma unroll
+    for (int st = 0; st < SMAX; ++st)
+      differ |= bits_of(a.st_start[own + (size_t)st * J]) != bits_of(E_in[prv + (size_t)st * J]);
+  bool active = (__builtin_amdgcn_ballot_w64(differ) & field) != 0 && valid;
+  const bool ran = active;
+  if (__builtin_amdgcn_ballot_w64(active) == 0) {
+    if (mine)
+#pragma unroll
+      for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = E_in[own + (size_t)st * J];
+    return;
+  }
+
+  // the models this lane's group hosts (re-running jobs only) and its configuration
+  const int p = valid ? job / a.K : 0;
+  int cfg = -1;
+  uint64_t hostbits = 0;  // bit m: this lane's group hosts model m
+  if (mine && ran) {
+    cfg = a.group_cfg[(int64_t)p * a.G + g];
+    if (cfg < 0 || cfg >= a.C) cfg = -1;  // an unused group hosts nothing
+    if (cfg >= 0) {
+      const uint64_t* hm = a.host_mask + (int64_t)p * a.M;
+      for (int m = 0; m < a.M; ++m) hostbits |= ((hm[m] >> g) & 1ull) << m;
+    }
+  }
+  int cp = 1, lshift = 0;
+  while (cp < a.C) cp <<= 1;
+  while ((1 << lshift) < cp * SMAX * 8) ++lshift;
+  unsigned char* rec = smem;
+  double* sL = reinterpret_cast<double*>(rec + (size_t)(a.M + 1) * (1 << RSH));  // [M][Cp][SMAX]
+  double* sT = sL + (size_t)a.M * cp * SMAX;                                    // arrivals, stride 2
+  uint32_t* sO = reinterpret_cast<uint32_t*>(sT + 128);                          // record offsets
+  const uint64_t vmask = __builtin_amdgcn_ballot_w64(cfg >= 0);
+  const int cfg0 = vmask ? __builtin_amdgcn_readlane(cfg, __builtin_ctzll(vmask)) : 0;
+  const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
+  for (int idx = lane; idx < a.M * cp * SMAX; idx += 64) {
+    const int st = idx % SMAX, mc = idx / SMAX, cc = mc % cp, m = mc / cp;
+    sL[idx] = cc < a.C ? a.stage_lat[((int64_t)m * a.C + cc) * a.smax_in + st] : 0.0;
+  }
+  for (int m = 0; m <= a.M; ++m) {
+    const uint64_t hm = m < a.M ? __builtin_amdgcn_ballot_w64((hostbits >> (m & 63)) & 1u) : 0;
+    if (lane == 0) {
+      const uint64_t one = lowest_per_field<W>(hm);  // lowest hosting lane of each job
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecMask) = hm;
+      *(uint64_t*)(rec + ((size_t)m << RSH) + kRecCount) = one == hm ? 0u : (uint32_t)__builtin_popcountll(one);
+    }
+  }
+  for (int m = lane; m <= a.M; m += 64) {
+    unsigned char* r = rec + ((size_t)m << RSH);
+    *(double*)(r + rec_slo(SMAX)) = m < a.M ? a.d_single[m] : 0.0;
+#pragma unroll
+    for (int st = 0; st < SMAX; ++st)
+      ((double*)(r + kRecLat))[st] =
+          (m < a.M && uni) ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + st] : 0.0;
+  }
+  SharedConst c;
+  c.rec = rec;
+  c.lrow = sL + (cfg < 0 ? 0 : cfg) * SMAX;
+  c.lshift = lshift;
+  c.sigma = valid ? a.slo_scale[job % a.K] : 0.0;
+  c.fmask = 0;
+  c.frowp = nullptr;
+  c.flimit = 0;
+  c.fcnt = 0;
+  c.cnt = nullptr;
+  SharedLane<SMAX> st;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) st.F[s] = (mine && ran) ? E_in[prv + (size_t)s * J] : 0.0;
+  st.fin_sum = st.hash = st.served = 0;  // served: the job's count, in every lane of it
+  st.wlo = 0;
+  st.busy = 0.0;
+  __syncthreads();
+
+  const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
+  const size_t ck0 = (size_t)k * a.ckps;
+  const int nck = b < e ? spec_ckpts(b, e, a.ck) : 0;
+  bool coupled = false;
+  TraceChunks tc;
+  tc.first(a, b, e, lane);
+  for (int64_t cb = b; cb < e; cb += 64) {
+    tc.advance(a, cb + 64, lane);
+    if (cb > b && (cb - b) % a.ck == 0) {
+      // saved state of the current results at cb: compare, then keep or stop
+      const int jl = (int)((cb - b) / a.ck) - 1;
+      const size_t j = ck0 + (size_t)jl;
+      bool same = true;
+      if (mine && active)
+#pragma unroll
+        for (int s = 0; s < SMAX; ++s)
+          same &= bits_of(a.ckpt[(j * GS + (size_t)g * SMAX + s) * J + job]) == bits_of(st.F[s]);
+      const bool job_same = (__builtin_amdgcn_ballot_w64(!same) & field) == 0;
+      const uint64_t js = st.served, jf = seg_sum_u64<W>(st.fin_sum);  // uniform flow
+      if (active) {
+        const size_t cj = j * J + job;
+        if (job_same) {
+          if (g == 0) {
+            const int64_t ds = (int64_t)js - a.ck_served[cj];
+            const uint64_t df = jf - a.ck_fsum[cj];
+            a.seg_served[(size_t)k * J + job] += ds;
+            a.seg_fsum[(size_t)k * J + job] += df;
+            a.ck_served[cj] = (int64_t)js;
+            a.ck_fsum[cj] = jf;
+            for (int j2 = jl + 1; j2 < nck; ++j2) {
+              a.ck_served[(ck0 + j2) * J + job] += ds;
+              a.ck_fsum[(ck0 + j2) * J + job] += df;
+            }
+          }
+          coupled = true;
+          active = false;
+        } else {
+          if (mine)
+#pragma unroll
+            for (int s = 0; s < SMAX; ++s) a.ckpt[(j * GS + (size_t)g * SMAX + s) * J + job] = st.F[s];
+          if (g == 0) {
+            a.ck_served[cj] = (int64_t)js;
+            a.ck_fsum[cj] = jf;
+          }
+        }
+      }
+      if (__builtin_amdgcn_ballot_w64(active) == 0) break;
+    }
+    if (cb - b >= a.cap && __builtin_amdgcn_ballot_w64(active) != 0) {
+      // runs from the two states do not meet: the pipeline gives up
+      if (lane == 0) a.cfg_info[2] = 1;
+      return;
+    }
+    const int cnt = __builtin_amdgcn_readfirstlane((int)(e - cb < 64 ? e - cb : 64));
+    // stage the chunk: lane r holds request cb + r
+    sT[2 * lane] = tc.tv;
+    sO[lane] = (uint32_t)((unsigned)tc.mv < (unsigned)a.M ? tc.mv : a.M) << RSH;
+    __syncthreads();
+    const uint64_t word = uni ? round_chunk<W, SMAX, true>(st, c, sT, sO, cnt)
+                              : round_chunk<W, SMAX, false>(st, c, sT, sO, cnt);
+    __syncthreads();
+    if (active && g == 0) a.bitmap[(cb >> 6) * J + job] = word;
+  }
+  const uint64_t js = st.served, jf = seg_sum_u64<W>(st.fin_sum);  // uniform flow
+  bool end_same = true;
+  if (mine && ran && !coupled)
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) end_same &= bits_of(E_in[own + (size_t)s * J]) == bits_of(st.F[s]);
+  const bool job_end_same = (__builtin_amdgcn_ballot_w64(!end_same) & field) == 0;
+  if (!valid) return;
+  if (ran) {
+    if (mine)
+#pragma unroll
+      for (int s = 0; s < SMAX; ++s) a.st_start[own + (size_t)s * J] = E_in[prv + (size_t)s * J];
+    if (!coupled) {
+      if (g == 0) {
+        a.seg_served[(size_t)k * J + job] = (int64_t)js;
+        a.seg_fsum[(size_t)k * J + job] = jf;
+      }
+      if (!job_end_same) {
+        if (mine)
+#pragma unroll
+          for (int s = 0; s < SMAX; ++s) E_out[own + (size_t)s * J] = st.F[s];
+        if (g == 0) atomicAdd(a.changed + q, 1);
+        return;
+      }
+    }
+  }
+  if (mine)
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) E_out[own + (size_t)s * J] = E_in[own + (size_t)s * J];
 }
 
 // Per job: totals over segments and the ordered digest over the accept words.
@@ -1216,13 +1447,15 @@ template <int W, int SMAX>
 void spec_rounds_gpl(const SpecArgs& a, hipStream_t s) {
   const int njbw = (a.J + 64 / W - 1) / (64 / W);
   const dim3 grid((unsigned)((int64_t)njbw * a.nseg)), block(64);
-  const size_t lds = (size_t)a.M * a.C * SMAX * 8;
   const bool full = spec_full<SMAX>(a);
+  int cp = 1;
+  while (cp < a.C) cp <<= 1;
+  const size_t lds = full ? round_fast_lds_bytes(a.M, cp, SMAX) : (size_t)a.M * a.C * SMAX * 8;
   for (int q = 1; q < a.nseg; ++q) {
     if (full)
-      hipLaunchKernelGGL((spec_round_gpl<W, SMAX, true>), grid, block, lds, s, a, q);
+      hipLaunchKernelGGL((spec_round_fast<W, SMAX>), grid, block, lds, s, a, q);
     else
-      hipLaunchKernelGGL((spec_round_gpl<W, SMAX, false>), grid, block, lds, s, a, q);
+      hipLaunchKernelGGL((spec_round_gpl<W, SMAX>), grid, block, lds, s, a, q);
   }
 }
 
