@@ -123,6 +123,8 @@ struct SharedConst {
   int64_t flimit;            // requests i < flimit have an output element
   int fcnt;                  // within a chunk: its first fcnt requests have one
   uint32_t* cnt;             // statistics launches: this job's per-model served counters (LDS)
+  uint32_t* cntw;            // statistics launches: the wavefront's counters, [job of the wavefront][M]
+  int M;                     // statistics launches: models (the counters' row length)
 };
 
 // Projection through this lane's stage chain (Sec. 3.4): fs[s] is the
@@ -175,14 +177,13 @@ __device__ __forceinline__ void fast_step(SharedLane<SMAX>& st, const SharedCons
   sr = (sr << 1) | (acc ? 1u : 0u);
   if constexpr (STATS) {
     // the accepting lane's group was busy for the model's slowest stage
-    // (fp64 sum in trace order) and served one more request of it
+    // (fp64 sum in trace order); the served counts per model are taken per
+    // 32 requests from the accept bits (fast_chunk)
     double slowest = 0.0;
 #pragma unroll
     for (int s = 0; s < SMAX; ++s) slowest = vmax(slowest, L[s]);
-    if (acc) {
-      st.busy += slowest;
-      atomicAdd(c.cnt + mi, 1u);
-    }
+    const double nb = st.busy + slowest;
+    st.busy = acc ? nb : st.busy;
   }
   if constexpr (FINISH) {
     // per-request output: the job's target lane writes the finish time, or
@@ -277,6 +278,18 @@ __device__ __forceinline__ void fast_chunk(SharedLane<SMAX>& st, const SharedCon
     // sr holds request e at bit hc-1-e; bits: request e at bit e
     const uint32_t bits =
         hc == 32 ? __builtin_bitreverse32(sr) : (__builtin_bitreverse32(sr) >> (32 - hc));
+    if constexpr (STATS) {
+      // served counts per model: lane e counts request h + e for every job
+      // of the wavefront that accepted it (integer counts: order-free)
+      const uint32_t jb = (uint32_t)seg_or<W>((uint64_t)bits);  // the job's bits, in every lane of it
+      const int e = (int)(threadIdx.x & 63);
+      const uint32_t me = e < hc ? (cO[h + e] >> rec_shift(SMAX)) : 0u;
+#pragma unroll
+      for (int j = 0; j < 64 / W; ++j) {
+        const uint32_t wj = (uint32_t)__builtin_amdgcn_readlane((int)jb, j * W);
+        if (e < hc && ((wj >> e) & 1u)) atomicAdd(c.cntw + j * c.M + me, 1u);
+      }
+    }
     if (pos == 0 && !end) {
       st.wlo = bits;
     } else {
@@ -428,6 +441,8 @@ __device__ __forceinline__ void shared_body(const KArgs& a, const JobSet& v, int
   if constexpr (STATS) {
     for (int idx = lane; idx < JW * a.M; idx += 64) sCnt[(size_t)wave * JW * a.M + idx] = 0;
     c.cnt = sCnt + ((size_t)wave * JW + lane / W) * a.M;
+    c.cntw = sCnt + (size_t)wave * JW * a.M;
+    c.M = a.M;
   }
 
   const int64_t n = a.n;

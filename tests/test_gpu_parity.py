@@ -206,6 +206,22 @@ def test_random_many_hosts(gpu, G):
             compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), n, f"many hosts G={G} S={S} n={n}")
 
 
+@pytest.mark.parametrize("G", [4, 16])
+def test_full_depth_mixed_configs(gpu, G):
+    """Every configuration equally deep but with latencies of its own, groups
+    of one job on different configurations: the reconciliation rounds' full-
+    depth kernel with per-lane latency rows (the cold-start and forced-segment
+    variants re-run most segments)."""
+    rng = np.random.default_rng(900 + G)
+    for S in (1, 2, 4):
+        n = int(rng.choice([2049, 6000]))
+        pb = _random_problem(rng, G, S, n, int(rng.integers(8, 40)), 2, mixed=True)
+        pb.cfg_stages[:] = S
+        say("full depth mixed", G, S, n, len(pb.cfg_stages))
+        res = gpu.simulate_problem(pb)
+        compare(res, oracle_problem(pb, finish_jobs=pb.finish_jobs), n, f"full depth G={G} S={S} n={n}")
+
+
 def test_tiny_cases_like_the_brute_force_pins(gpu):
     """The random tiny problems the oracle's brute-force pin uses, one call each."""
     from paper_2302_11665_amd.workload.problems import Problem
