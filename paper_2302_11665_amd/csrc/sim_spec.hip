@@ -246,7 +246,7 @@ template <int SMAX, bool UCFG>
 struct SpecLds {
   double* T;      // UCFG: [M][SMAX + 1]; else L: [M][C][SMAX]
   double* D;      // !UCFG: [M]
-  uint16_t* cfg;  // !UCFG: [G][JPW] = c | S << 8
+  uint16_t* cfg;  // !UCFG: [G][JPW] = c
   double* F;      // rows -1 .. G of [SMAX][JPW]; row -1 is a sentinel, row G is written, never read
 };
 
@@ -300,7 +300,7 @@ __device__ __forceinline__ SpecLds<SMAX, UCFG> spec_tables(const SpecArgs& a, do
       for (int g = 0; g < a.G; ++g) {
         int c = valid ? a.group_cfg[(int64_t)p * a.G + g] : -1;
         if (c < 0 || c >= C) c = 0;  // a group hosting nothing is never chosen
-        s.cfg[g * JPW + lane] = (uint16_t)(c | (a.cfg_stages[c] << 8));
+        s.cfg[g * JPW + lane] = (uint16_t)c;
       }
   }
   // the sentinel row: stage 0 never wins, the other stages are never committed
@@ -394,13 +394,11 @@ __device__ __forceinline__ Reads<SMAX, UCFG> issue_reads(const SpecLds<SMAX, UCF
 // commit of one request on the lane's state.  Returns whether the request is
 // served (never on an inactive lane); out is its finish time (-1 dropped, -2
 // no hosting group).  Requests that are not served write the spare row G.
-// X as for issue_reads (rd.extra: the extra hosts were read).  FULL: every
-// group has SMAX stages (a uniform configuration of the deepest kind).
-template <int SMAX, bool UCFG, int MB, int JPW, int X, bool FULL>
+// X as for issue_reads (rd.extra: the extra hosts were read).
+template <int SMAX, bool UCFG, int MB, int JPW, int X>
 __device__ __forceinline__ bool finish_step(const SpecLds<SMAX, UCFG>& s, const Plan<MB>& pl,
                                             const Reads<SMAX, UCFG>& rd, int lane, double scale, int C, int G,
-                                            int S0, bool active, double& out) {
-  static_assert(!FULL || UCFG, "FULL needs a uniform configuration");
+                                            bool active, double& out) {
   constexpr int kX = Reads<SMAX, UCFG>::kX;
   // g1 > g0, and further hosts come in increasing order: strict comparisons
   // keep the lowest index among equal free times (a missing host is the
@@ -440,36 +438,25 @@ __device__ __forceinline__ bool finish_step(const SpecLds<SMAX, UCFG>& s, const 
     }
   }
   double Lv[SMAX];
-  int S = S0;
   if constexpr (UCFG) {
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) Lv[k] = rd.L[k];
   } else {
-    const uint32_t e = s.cfg[(g < 0 ? 0 : g) * JPW + lane];
-    const int c = (int)(e & 0xFF);
-    S = (int)(e >> 8);
+    const int c = s.cfg[(g < 0 ? 0 : g) * JPW + lane];
     const int mi = (unsigned)pl.m < 64u ? pl.m : 0;
     const double* Lrow = s.T + ((size_t)mi * C + c) * SMAX;
 #pragma unroll
     for (int k = 0; k < SMAX; ++k) Lv[k] = Lrow[k];
   }
-  // projection through the stage chain; stages past S keep their state
+  // projection through the stage chain.  A stage past the group's depth has
+  // zero latency: its free time is always the last real stage's (so at most
+  // the new finish time), and the finish time passes it unchanged.
   double f[SMAX];
   double prev = pl.t;
-  if (FULL || (UCFG && S == SMAX)) {
 #pragma unroll
-    for (int k = 0; k < SMAX; ++k) {
-      f[k] = vmax(prev, Fv[k]) + Lv[k];
-      prev = f[k];
-    }
-  } else {
-#pragma unroll
-    for (int k = 0; k < SMAX; ++k) {
-      const double x = vmax(prev, Fv[k]) + Lv[k];
-      const bool in = k < S;
-      f[k] = in ? x : Fv[k];
-      prev = in ? x : prev;
-    }
+  for (int k = 0; k < SMAX; ++k) {
+    f[k] = vmax(prev, Fv[k]) + Lv[k];
+    prev = f[k];
   }
   const double slo = scale * rd.d;
   const double deadline = pl.t + slo;
@@ -533,11 +520,9 @@ struct TraceChunks {
 // (on an inactive lane with served false and out meaningless; rows: the chunk
 // writes finish rows), after a placeholder call per chunk (i = base - 1,
 // served and rows false), chunk_end(base, cnt) closes the chunk.
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL, bool ROWS, class Begin, class Result,
-          class End>
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool ROWS, class Begin, class Result, class End>
 __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX, UCFG>& s,
-                                           const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int S0,
-                                           int64_t from, int64_t to, const bool& active, Begin chunk_begin,
+                                           const LaneMasks<MB>& msk, const SpecLane& ln, int lane, int64_t from, int64_t to, const bool& active, Begin chunk_begin,
                                            Result result, End chunk_end) {
   if (from >= to) return;
   const int li = lane & (JPW - 1);  // lanes past JPW hold no job: they read a valid lane's slot
@@ -581,8 +566,7 @@ __device__ __forceinline__ void spec_range(const SpecArgs& a, const SpecLds<SMAX
       const double t_nx =
           __hiloint2double(__builtin_amdgcn_readlane(t1_hi, r), __builtin_amdgcn_readlane(t1_lo, r));
       const Plan<MB> nxt = make_plan<MB>(a, msk, t_nx, __builtin_amdgcn_readlane(m1, r));
-      served_p = finish_step<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0, FULL>(s, cur, rd, li, ln.scale, a.C, a.G, S0,
-                                                                       active, out_p);
+      served_p = finish_step<SMAX, UCFG, MB, JPW, EXTRA ? 2 : 0>(s, cur, rd, li, ln.scale, a.C, a.G, active, out_p);
       cur = nxt;
     }
     result(cb + cnt - 1, cnt - 1, out_p, served_p, rows);
@@ -595,7 +579,7 @@ __device__ __forceinline__ int spec_ckpts(int64_t b, int64_t e, int64_t ck) { re
 
 // Pass 0 of one wavefront (the per-request output rows are written by
 // spec_rows once the rounds have made every saved state exact).
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA>
 __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, int lane, int k,
                                                 const SpecLane& ln, int c0) {
   LaneMasks<MB> msk;
@@ -604,7 +588,6 @@ __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, 
   const int GS = a.G * SMAX;
   if (lane < JPW)
     for (int q = 0; q < GS; ++q) s.F[q * JPW + lane] = 0.0;
-  const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   if (blockIdx.x == 0 && lane < a.nseg) a.changed[lane] = lane == 0 ? 1 : 0;
 
   const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
@@ -621,8 +604,8 @@ __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, 
   const size_t ck0 = (size_t)k * a.ckps;
   if (w0 == b && ln.valid)
     for (int q = 0; q < GS; ++q) a.st_start[seg_base + (size_t)q * J] = 0.0;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA, FULL, false>(
-      a, s, msk, ln, lane, S0, w0, e, on,
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, false>(
+      a, s, msk, ln, lane, w0, e, on,
       [&](int64_t cb) {
         if (cb == b) {
           // the warm-up counts nothing
@@ -672,10 +655,8 @@ __device__ __forceinline__ void spec_pass0_body(const SpecArgs& a, double* lds, 
 // four variants, all launched: UCFG (all groups of all placements share one
 // configuration) and EXTRA (some lane of the wavefront hosts a model on more
 // than two groups) select the code; a workgroup whose data do not match its
-// variant returns at once, before any side effect.  FULL (every
-// configuration has SMAX stages, so a uniform one runs the whole chain) is
-// chosen on the host.
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
+// variant returns at once, before any side effect.
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA>
 __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
   if ((a.cfg_info[0] != 0) != UCFG) return;
   const int c0 = UCFG ? a.cfg_info[1] : 0;
@@ -689,7 +670,7 @@ __global__ __launch_bounds__(64) void spec_pass0(const SpecArgs a) {
     const bool many = m0.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
     if ((__builtin_amdgcn_ballot_w64(many) != 0) != EXTRA) return;
   }
-  spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA, FULL>(a, lds, lane, k, ln, c0);
+  spec_pass0_body<SMAX, MB, UCFG, JPW, EXTRA>(a, lds, lane, k, ln, c0);
 }
 
 // Per job: served counts and finish-time sums over the segments, and the
@@ -742,7 +723,7 @@ __device__ __forceinline__ void final_body(const SpecArgs& a, int64_t job) {
 // The extra-host code (some lane hosts a model on more than two groups) is
 // chosen per wavefront at run time, so that every row piece, and the final
 // step in the dispatch's first nfb workgroups, run in one dispatch.
-template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA, bool FULL>
+template <int SMAX, int MB, bool UCFG, int JPW, bool EXTRA>
 __device__ __forceinline__ void rows_body(const SpecArgs& a, double* lds, int lane, const SpecLane& ln, int c0,
                                           int k, int pc, int64_t pb, int64_t pe) {
   LaneMasks<MB> msk;  // loaded again here: one copy per body keeps it in registers
@@ -755,10 +736,9 @@ __device__ __forceinline__ void rows_body(const SpecArgs& a, double* lds, int la
       s.F[q * JPW + lane] = !ln.valid ? 0.0
                             : pc == 0 ? a.st_start[((size_t)k * GS + q) * J + ln.job]
                                       : a.ckpt[(((size_t)k * a.ckps + pc - 1) * GS + q) * J + ln.job];
-  const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   const bool on = true;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA, FULL, true>(
-      a, s, msk, ln, lane, S0, pb, pe, on, [](int64_t) { return 2; },
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, true>(
+      a, s, msk, ln, lane, pb, pe, on, [](int64_t) { return 2; },
       [&](int64_t i, int r, double out, bool sv, bool rows) {
         (void)r;
         (void)sv;
@@ -767,7 +747,7 @@ __device__ __forceinline__ void rows_body(const SpecArgs& a, double* lds, int la
       [](int64_t, int) {});
 }
 
-template <int SMAX, int MB, bool UCFG, int JPW, bool FULL>
+template <int SMAX, int MB, bool UCFG, int JPW>
 __global__ __launch_bounds__(64) void spec_rows(const SpecArgs a, int nfb) {
   if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels write the rows
   if ((a.cfg_info[0] != 0) != UCFG) return;
@@ -801,9 +781,9 @@ __global__ __launch_bounds__(64) void spec_rows(const SpecArgs a, int nfb) {
     many = msk.load(a.host_mask + (int64_t)ln.p * a.M, a.M, a.G, ln.valid);
   }
   if (__builtin_amdgcn_ballot_w64(many) != 0)
-    rows_body<SMAX, MB, UCFG, JPW, true, FULL>(a, lds, lane, ln, c0, k, pc, pb, pe);
+    rows_body<SMAX, MB, UCFG, JPW, true>(a, lds, lane, ln, c0, k, pc, pb, pe);
   else
-    rows_body<SMAX, MB, UCFG, JPW, false, FULL>(a, lds, lane, ln, c0, k, pc, pb, pe);
+    rows_body<SMAX, MB, UCFG, JPW, false>(a, lds, lane, ln, c0, k, pc, pb, pe);
 }
 
 // Round q >= 1: a segment whose start state differs from its predecessor's
@@ -845,7 +825,6 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
     return;
   }
   const auto s = spec_tables<SMAX, UCFG, JPW>(a, lds, lane, ln.p, ln.valid, c0);
-  const int S0 = UCFG ? a.cfg_stages[c0] : 0;
   if (lane < JPW)
     for (int x = 0; x < GS; ++x) s.F[x * JPW + lane] = active ? E_in[prv + (size_t)x * J] : 0.0;
 
@@ -855,8 +834,8 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   int64_t served = 0;
   uint64_t fsum = 0, word = 0;
   bool coupled = false, gave_up = false;
-  spec_range<SMAX, MB, UCFG, JPW, EXTRA, false, false>(
-      a, s, msk, ln, lane, S0, b, e, active,
+  spec_range<SMAX, MB, UCFG, JPW, EXTRA, false>(
+      a, s, msk, ln, lane, b, e, active,
       [&](int64_t cb) {
         if (cb > b && (cb - b) % a.ck == 0 && active) {
           const int jl = (int)((cb - b) / a.ck) - 1;
@@ -931,228 +910,6 @@ __global__ __launch_bounds__(64) void spec_round(const SpecArgs a, int q) {
   for (int x = 0; x < GS; ++x) E_out[own + (size_t)x * J] = E_in[own + (size_t)x * J];
 }
 
-// Unsigned minimum over each aligned group of W <= 16 lanes, in every lane of
-// it: one v_min_u32 with a DPP operand per halving step.  Every lane of the
-// group must be active.
-template <int W>
-__device__ __forceinline__ uint32_t seg_min_u32w(uint32_t x) {
-  static_assert(W <= 16, "row-local steps only");
-  auto umin = [](uint32_t p, uint32_t q) { return p < q ? p : q; };
-  if constexpr (W >= 2) x = umin(x, dpp_u32<kXor1>(x));
-  if constexpr (W >= 4) x = umin(x, dpp_u32<kXor2>(x));
-  if constexpr (W >= 8) x = umin(x, dpp_u32<kHalfMirror>(x));
-  if constexpr (W >= 16) x = umin(x, dpp_u32<kMirror>(x));
-  return x;
-}
-
-// Round q >= 1 in the group-per-lane layout (jobs of at most 16 groups): the
-// same protocol as spec_round, but a job has W lanes, one group each, with its
-// stage free times in registers and the dispatch a DPP min over the W lanes.
-// A round re-runs only a few jobs, and its time is the longest re-run: per
-// request this layout has a shorter dependency chain than one lane per job.
-// This kernel serves placements with configurations of fewer than SMAX
-// stages (a stage past a group's depth keeps its free time, as in pass 0);
-// spec_round_fast the rest.  A lane collects the accept bits of the requests
-// it commits; the job's word is their OR over its W lanes once per chunk.
-template <int W, int SMAX>
-__global__ __launch_bounds__(64) void spec_round_gpl(const SpecArgs a, int q) {
-  constexpr int JW = 64 / W;  // jobs per wavefront
-  if (a.cfg_info[2] != 0) return;  // a re-run gave up: other kernels take over
-  if (a.changed[q - 1] == 0) return;
-  extern __shared__ double lds[];
-  const int lane = threadIdx.x;
-  const int g = lane % W, slot = lane / W;
-  const int njbw = (a.J + JW - 1) / JW;
-  const int k = blockIdx.x / njbw, jb = blockIdx.x % njbw;
-  const int job = jb * JW + slot;
-  const bool valid = job < a.J;
-  const bool mine = valid && g < a.G;  // this lane holds a group of a job
-  const int GS = a.G * SMAX;
-  const int64_t J = a.J;
-  const size_t per_buf = (size_t)a.nseg * GS * J;
-  const double* E_in = a.st_end + (size_t)((q - 1) & 1) * per_buf;
-  double* E_out = a.st_end + (size_t)(q & 1) * per_buf;
-  const size_t own = ((size_t)k * GS + (size_t)g * SMAX) * J + job;  // my group's first entry
-  const size_t prv = k > 0 ? ((size_t)(k - 1) * GS + (size_t)g * SMAX) * J + job : 0;
-  const uint64_t fbase = (uint64_t)slot * W;
-  const uint64_t field = (W == 64 ? ~0ull : ((1ull << W) - 1)) << fbase;
-  const uint64_t below = ((1ull << lane) - 1) & field;
-
-  // stale start state?  (every lane of a job agrees through the ballot)
-  bool differ = false;
-  if (mine && k > 0)
-#pragma unroll
-    for (int st = 0; st < SMAX; ++st)
-      differ |= bits_of(a.st_start[own + (size_t)st * J]) != bits_of(E_in[prv + (size_t)st * J]);
-  bool active = (__builtin_amdgcn_ballot_w64(differ) & field) != 0 && valid;
-  const bool ran = active;
-  if (__builtin_amdgcn_ballot_w64(active) == 0) {
-    if (mine)
-#pragma unroll
-      for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = E_in[own + (size_t)st * J];
-    return;
-  }
-  // per-lane data: the models my group hosts, its configuration and depth,
-  // the job's scale, the stage-latency table in LDS, d_single by lane
-  const int p = valid ? job / a.K : 0;
-  const double scale = valid ? a.slo_scale[job % a.K] : 0.0;
-  uint64_t hostm = 0;
-  int cg = 0, Sg = 1;
-  if (mine) {
-    for (int m = 0; m < a.M; ++m) hostm |= ((a.host_mask[(int64_t)p * a.M + m] >> g) & 1ull) << m;
-    cg = a.group_cfg[(int64_t)p * a.G + g];
-    if (cg < 0 || cg >= a.C) {
-      cg = 0;
-      hostm = 0;  // an unused group hosts nothing
-    }
-    Sg = a.cfg_stages[cg];
-  }
-  double* Lt = lds;  // [M][C][SMAX]
-  for (int e = lane; e < a.M * a.C * SMAX; e += 64) {
-    const int st = e % SMAX, c = (e / SMAX) % a.C, m = e / (SMAX * a.C);
-    Lt[e] = st < a.cfg_stages[c] ? a.stage_lat[((int64_t)m * a.C + c) * a.smax_in + st] : 0.0;
-  }
-  const double dl_lane = lane < a.M ? a.d_single[lane] : 1.0;
-  __syncthreads();
-  double F[SMAX];
-#pragma unroll
-  for (int st = 0; st < SMAX; ++st) F[st] = (mine && active) ? E_in[prv + (size_t)st * J] : 0.0;
-
-  const int64_t b = seg_bound(a.n, a.nseg, k), e = seg_bound(a.n, a.nseg, k + 1);
-  const size_t ck0 = (size_t)k * a.ckps;
-  const int nck = b < e ? spec_ckpts(b, e, a.ck) : 0;
-  uint64_t served = 0, fsum = 0;  // this lane's share (the requests it committed)
-  bool coupled = false;
-  TraceChunks tc;
-  tc.first(a, b, e, lane);
-  for (int64_t cb = b; cb < e; cb += 64) {
-    tc.advance(a, cb + 64, lane);
-    if (cb > b && (cb - b) % a.ck == 0) {
-      // saved state of the current results at cb: compare, then keep or stop
-      const int jl = (int)((cb - b) / a.ck) - 1;
-      const size_t j = ck0 + (size_t)jl;
-      bool same = true;
-      if (mine && active)
-#pragma unroll
-        for (int st = 0; st < SMAX; ++st)
-          same &= bits_of(a.ckpt[(j * GS + (size_t)g * SMAX + st) * J + job]) == bits_of(F[st]);
-      const bool job_same = (__builtin_amdgcn_ballot_w64(!same) & field) == 0;
-      const uint64_t js = seg_sum_u64<W>(served), jf = seg_sum_u64<W>(fsum);  // uniform flow
-      if (active) {
-        const size_t cj = j * J + job;
-        if (job_same) {
-          if (g == 0) {
-            const int64_t ds = (int64_t)js - a.ck_served[cj];
-            const uint64_t df = jf - a.ck_fsum[cj];
-            a.seg_served[(size_t)k * J + job] += ds;
-            a.seg_fsum[(size_t)k * J + job] += df;
-            a.ck_served[cj] = (int64_t)js;
-            a.ck_fsum[cj] = jf;
-            for (int j2 = jl + 1; j2 < nck; ++j2) {
-              a.ck_served[(ck0 + j2) * J + job] += ds;
-              a.ck_fsum[(ck0 + j2) * J + job] += df;
-            }
-          }
-          coupled = true;
-          active = false;
-        } else {
-          if (mine)
-#pragma unroll
-            for (int st = 0; st < SMAX; ++st) a.ckpt[(j * GS + (size_t)g * SMAX + st) * J + job] = F[st];
-          if (g == 0) {
-            a.ck_served[cj] = (int64_t)js;
-            a.ck_fsum[cj] = jf;
-          }
-        }
-      }
-      if (__builtin_amdgcn_ballot_w64(active) == 0) break;
-    }
-    if (cb - b >= a.cap && __builtin_amdgcn_ballot_w64(active) != 0) {
-      // runs from the two states do not meet: the pipeline gives up
-      if (lane == 0) a.cfg_info[2] = 1;
-      return;
-    }
-    const int cnt = __builtin_amdgcn_readfirstlane((int)(e - cb < 64 ? e - cb : 64));
-    uint64_t lw = 0;  // accept bits of the requests this lane committed
-    for (int r = 0; r < cnt; ++r) {
-      const double ti = readlane_f64(tc.tv, r);
-      const int m = __builtin_amdgcn_readlane(tc.mv, r);
-      if (!active) continue;
-      const bool host = (unsigned)m < (unsigned)a.M && ((hostm >> (m & 63)) & 1ull);
-      const int mi = (unsigned)m < (unsigned)a.M ? m : 0;
-      double L[SMAX];
-#pragma unroll
-      for (int st = 0; st < SMAX; ++st) L[st] = Lt[((size_t)mi * a.C + cg) * SMAX + st];
-      // dispatch on the free times' bit patterns: they are >= 0 (the sign
-      // bit cleared merges -0 with +0), so the unsigned order of the patterns
-      // is the numeric order; lanes not hosting m take all ones.  The high
-      // words first, the low words only where two lanes of a job tie on the
-      // high word.  (The cross-lane minima are taken in every lane, never
-      // behind a lane condition: a lane left out would read as zero.)
-      const uint64_t kb = bits_of(F[0]);
-      const uint32_t kh = host ? (uint32_t)(kb >> 32) & 0x7FFFFFFFu : 0xFFFFFFFFu;
-      const uint32_t mh = seg_min_u32w<W>(kh);
-      bool eq = host && kh == mh;
-      uint64_t ball = __builtin_amdgcn_ballot_w64(eq);
-      if (__builtin_amdgcn_ballot_w64(eq && (ball & below) != 0) != 0) {
-        const uint32_t kl = eq ? (uint32_t)kb : 0xFFFFFFFFu;
-        const uint32_t ml = seg_min_u32w<W>(kl);
-        eq = eq && kl == ml;
-        ball = __builtin_amdgcn_ballot_w64(eq);
-      }
-      const bool chosen = eq && (ball & below) == 0;
-      double f[SMAX];
-      double prev = ti;
-#pragma unroll
-      for (int st = 0; st < SMAX; ++st) {
-        const double x = vmax(prev, F[st]) + L[st];
-        const bool in = st < Sg;
-        f[st] = in ? x : F[st];
-        prev = in ? x : prev;
-      }
-      const double deadline = ti + scale * readlane_f64(dl_lane, mi);
-      const bool acc = chosen && !(prev > deadline);
-      if (acc) {
-#pragma unroll
-        for (int st = 0; st < SMAX; ++st) F[st] = f[st];
-        served += 1;
-        fsum += bits_of(prev);
-        lw |= 1ull << r;
-      }
-    }
-    const uint64_t word = seg_or<W>(lw);  // every lane: the word of its job
-    if (active && g == 0) a.bitmap[(cb >> 6) * J + job] = word;
-  }
-  const uint64_t js = seg_sum_u64<W>(served), jf = seg_sum_u64<W>(fsum);  // uniform flow
-  bool end_same = true;
-  if (mine && ran && !coupled)
-#pragma unroll
-    for (int st = 0; st < SMAX; ++st) end_same &= bits_of(E_in[own + (size_t)st * J]) == bits_of(F[st]);
-  const bool job_end_same = (__builtin_amdgcn_ballot_w64(!end_same) & field) == 0;
-  if (!valid) return;
-  if (ran) {
-    if (mine)
-#pragma unroll
-      for (int st = 0; st < SMAX; ++st) a.st_start[own + (size_t)st * J] = E_in[prv + (size_t)st * J];
-    if (!coupled) {
-      if (g == 0) {
-        a.seg_served[(size_t)k * J + job] = (int64_t)js;
-        a.seg_fsum[(size_t)k * J + job] = jf;
-      }
-      if (!job_end_same) {
-        if (mine)
-#pragma unroll
-          for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = F[st];
-        if (g == 0) atomicAdd(a.changed + q, 1);
-        return;
-      }
-    }
-  }
-  if (mine)
-#pragma unroll
-    for (int st = 0; st < SMAX; ++st) E_out[own + (size_t)st * J] = E_in[own + (size_t)st * J];
-}
-
 // One 64-request chunk (cnt <= 64 of them, staged in LDS) of a round in the
 // group-per-lane layout, run by the shared-trace kernel's request step;
 // returns the job's accept word (request r at bit r, in every lane of the
@@ -1186,16 +943,19 @@ __host__ __device__ constexpr size_t round_fast_lds_bytes(int M, int Cp, int SMA
   return (size_t)(M + 1) * ((size_t)1 << rec_shift(SMAX)) + (size_t)M * Cp * SMAX * 8 + 128 * 8 + 64 * 4;
 }
 
-// Round q >= 1 in the group-per-lane layout where every configuration has
-// SMAX stages: the protocol of spec_round_gpl with the shared-trace kernel's
-// request step -- per-wavefront model records in LDS (hosting lanes, the
-// count that says whether a dispatch minimum is needed, stage latencies,
-// d_single), the two-level integer minimum, four requests' inputs read
-// together -- which issues about half the instructions per request of the
-// lane-by-lane step.  Only the jobs that re-run host models in the records; a
-// job that has met the old results keeps simulating with the others but
-// writes nothing more.  Each 64-request chunk is staged in LDS from registers
-// loaded a chunk ahead.
+// Round q >= 1 in the group-per-lane layout (jobs of at most 16 groups): the
+// protocol of spec_round with a job's groups on W lanes, their stage free
+// times in registers, and the shared-trace kernel's request step --
+// per-wavefront model records in LDS (hosting lanes, the count that says
+// whether a dispatch minimum is needed, stage latencies, d_single), the
+// two-level integer minimum, four requests' inputs read together.  A round
+// re-runs few jobs and lasts as long as its longest re-run, and per request
+// this layout is a shorter chain than one lane per job.  Stages past a
+// group's depth have zero latency, as in the other speculative kernels, so
+// saved states compare bit for bit.  Only the jobs that re-run host models in
+// the records; a job that has met the old results keeps simulating with the
+// others but writes nothing more.  Each 64-request chunk is staged in LDS
+// from registers loaded a chunk ahead.
 template <int W, int SMAX>
 __global__ __launch_bounds__(64) void spec_round_fast(const SpecArgs a, int q) {
   constexpr int JW = 64 / W;  // jobs per wavefront
@@ -1258,7 +1018,7 @@ __global__ __launch_bounds__(64) void spec_round_fast(const SpecArgs a, int q) {
   const bool uni = __builtin_amdgcn_ballot_w64(cfg >= 0 && cfg != cfg0) == 0;
   for (int idx = lane; idx < a.M * cp * SMAX; idx += 64) {
     const int st = idx % SMAX, mc = idx / SMAX, cc = mc % cp, m = mc / cp;
-    sL[idx] = cc < a.C ? a.stage_lat[((int64_t)m * a.C + cc) * a.smax_in + st] : 0.0;
+    sL[idx] = (cc < a.C && st < a.cfg_stages[cc]) ? a.stage_lat[((int64_t)m * a.C + cc) * a.smax_in + st] : 0.0;
   }
   for (int m = 0; m <= a.M; ++m) {
     const uint64_t hm = m < a.M ? __builtin_amdgcn_ballot_w64((hostbits >> (m & 63)) & 1u) : 0;
@@ -1274,7 +1034,8 @@ __global__ __launch_bounds__(64) void spec_round_fast(const SpecArgs a, int q) {
 #pragma unroll
     for (int st = 0; st < SMAX; ++st)
       ((double*)(r + kRecLat))[st] =
-          (m < a.M && uni) ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + st] : 0.0;
+          (m < a.M && uni && st < a.cfg_stages[cfg0]) ? a.stage_lat[((int64_t)m * a.C + cfg0) * a.smax_in + st]
+                                                      : 0.0;
   }
   SharedConst c;
   c.rec = rec;
@@ -1433,30 +1194,15 @@ __global__ __launch_bounds__(1024) void spec_cfg_check(const int32_t* group_cfg,
   }
 }
 
-// Whether every configuration has SMAX stages: a uniform configuration is
-// then the deepest kind, and pass 0 and the rounds run every stage of the chain.
-template <int SMAX>
-bool spec_full(const SpecArgs& a) {
-  for (int c = 0; c < a.C; ++c)
-    if (a.cfg_stages[c] != SMAX) return false;
-  return true;
-}
-
 // Rounds in the group-per-lane layout (jobs of at most 16 groups).
 template <int W, int SMAX>
 void spec_rounds_gpl(const SpecArgs& a, hipStream_t s) {
   const int njbw = (a.J + 64 / W - 1) / (64 / W);
   const dim3 grid((unsigned)((int64_t)njbw * a.nseg)), block(64);
-  const bool full = spec_full<SMAX>(a);
   int cp = 1;
   while (cp < a.C) cp <<= 1;
-  const size_t lds = full ? round_fast_lds_bytes(a.M, cp, SMAX) : (size_t)a.M * a.C * SMAX * 8;
-  for (int q = 1; q < a.nseg; ++q) {
-    if (full)
-      hipLaunchKernelGGL((spec_round_fast<W, SMAX>), grid, block, lds, s, a, q);
-    else
-      hipLaunchKernelGGL((spec_round_gpl<W, SMAX>), grid, block, lds, s, a, q);
-  }
+  const size_t lds = round_fast_lds_bytes(a.M, cp, SMAX);
+  for (int q = 1; q < a.nseg; ++q) hipLaunchKernelGGL((spec_round_fast<W, SMAX>), grid, block, lds, s, a, q);
 }
 
 template <int SMAX>
@@ -1474,15 +1220,10 @@ void spec_rounds_gpl_w(const SpecArgs& a, hipStream_t s) {
 template <int SMAX, int MB, int JPW>
 hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStream_t s) {
   const dim3 grid((unsigned)((int64_t)a.njb * a.nseg)), block(64);
-  if (spec_full<SMAX>(a)) {
-    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false, true>), grid, block, lds_u, s, a);
-    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true, true>), grid, block, lds_u, s, a);
-  } else {
-    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false, false>), grid, block, lds_u, s, a);
-    hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true, false>), grid, block, lds_u, s, a);
-  }
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, false, false>), grid, block, lds_g, s, a);
-  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, true, false>), grid, block, lds_g, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, false>), grid, block, lds_u, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, true, JPW, true>), grid, block, lds_u, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, false>), grid, block, lds_g, s, a);
+  hipLaunchKernelGGL((spec_pass0<SMAX, MB, false, JPW, true>), grid, block, lds_g, s, a);
   if (a.G <= 16 && spec_gpl_rounds()) {
     spec_rounds_gpl_w<SMAX>(a, s);
   } else {
@@ -1498,11 +1239,8 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
     // the output rows, from the exact saved states, all pieces at once, and
     // in the same dispatch (its first nfb workgroups) the final step
     const dim3 rgrid((unsigned)(nfb + (int64_t)((a.n_finish + JPW - 1) / JPW) * a.nseg * (a.ckps + 1)));
-    if (spec_full<SMAX>(a))
-      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, true>), rgrid, block, lds_u, s, a, nfb);
-    else
-      hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW, false>), rgrid, block, lds_u, s, a, nfb);
-    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW, false>), rgrid, block, lds_g, s, a, nfb);
+    hipLaunchKernelGGL((spec_rows<SMAX, MB, true, JPW>), rgrid, block, lds_u, s, a, nfb);
+    hipLaunchKernelGGL((spec_rows<SMAX, MB, false, JPW>), rgrid, block, lds_g, s, a, nfb);
   } else {
     hipLaunchKernelGGL(spec_final, dim3((unsigned)nfb), block, 0, s, a);
   }
@@ -1514,7 +1252,7 @@ hipError_t spec_launch_all(const SpecArgs& a, size_t lds_u, size_t lds_g, hipStr
 template <int SMAX, int MB, int JPW>
 int spec_occupancy(size_t lds) {
   int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW, false, false>, 64, lds) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, spec_pass0<SMAX, MB, true, JPW, false>, 64, lds) != hipSuccess)
     return 1;
   return nb > 0 ? nb : 1;
 }
