@@ -60,19 +60,19 @@ KERNEL_SOURCES = ["paper_2302_11665_amd/csrc/sim_api.hip", "paper_2302_11665_amd
                   "paper_2302_11665_amd/csrc/sim_launch.hip", "paper_2302_11665_amd/csrc/sim_launch.hpp",
                   "paper_2302_11665_amd/csrc/sim_shared.hpp", "paper_2302_11665_amd/csrc/sim_spec.hip"]
 MEASURED_TRAFFIC = {
-    "sources_sha256": "84f44ab98b84f4f8c7337d5521e2116e17bc81153f8a6ac08759dd33375f82a4",
+    "sources_sha256": "684637c3137697b219070a57f8d6c86345014f155cb72e55f014cddc6114a889",
     # one step of the heavy-trace workload runs the segment-speculative
     # pipeline (configuration check, pass 0, reconciliation rounds, output
     # rows, digest): its counters summed over the step's dispatches
-    "kernel": "spec_pass0<4, 32, true, 64, true, true> + spec_round_fast<16, 4> + spec_rows<4, 32, true, 64, "
-              "true> (row pieces and the final step) + spec_cfg_check (+ the variants that return at once)",
-    "fetch_kib": 2216553.75, "write_kib": 5990709.97,
+    "kernel": "spec_pass0<4, 32, true, 64, true> + spec_round_fast<16, 4> + spec_rows<4, 32, true, 64> "
+              "(row pieces and the final step) + spec_cfg_check (+ the variants that return at once)",
+    "fetch_kib": 2218171.63, "write_kib": 5990707.06,
     "fetch_scale": 1048576.0 / 524301.90, "write_scale": 1048576.0 / 1048576.0,
 }
 MEASURED_TRAFFIC_SWEEP = {
-    "sources_sha256": "84f44ab98b84f4f8c7337d5521e2116e17bc81153f8a6ac08759dd33375f82a4",
+    "sources_sha256": "684637c3137697b219070a57f8d6c86345014f155cb72e55f014cddc6114a889",
     "kernel": "seg_kernel<1>",
-    "fetch_kib": 2595530.31, "write_kib": 14216.28,
+    "fetch_kib": 2595524.38, "write_kib": 14218.69,
     "fetch_scale": 1048576.0 / 524301.90, "write_scale": 1048576.0 / 1048576.0,
 }
 
