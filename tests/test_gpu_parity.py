@@ -209,9 +209,9 @@ def test_random_many_hosts(gpu, G):
 @pytest.mark.parametrize("G", [4, 16])
 def test_full_depth_mixed_configs(gpu, G):
     """Every configuration equally deep but with latencies of its own, groups
-    of one job on different configurations: the reconciliation rounds' full-
-    depth kernel with per-lane latency rows (the cold-start and forced-segment
-    variants re-run most segments)."""
+    of one job on different configurations: the reconciliation rounds'
+    per-lane latency rows with no stage past any group's depth (the
+    cold-start and forced-segment variants re-run most segments)."""
     rng = np.random.default_rng(900 + G)
     for S in (1, 2, 4):
         n = int(rng.choice([2049, 6000]))
