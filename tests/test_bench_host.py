@@ -71,3 +71,13 @@ def test_more_than_one_gpu_is_refused(argv, env):
                        env=e, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stdout
+
+
+def test_sweep_algorithmic_bytes_hand_count():
+    from types import SimpleNamespace
+    # 3 segments of 4, 0 and 5 requests, 4 jobs, 2 output rows of stride 5
+    sp = SimpleNamespace(t=np.zeros(9), seg_offsets=np.array([0, 4, 4, 9], np.int64),
+                         job_segment=np.array([0, 1, 2, 2], np.int32))
+    # every request read once (12 B), the offsets, a 16-byte job record and
+    # 32 bytes of outputs per job, and the output rows
+    assert bench.sweep_algorithmic_bytes(sp, 2, 5) == 12 * 9 + 4 * 8 + 16 * 4 + 32 * 4 + 8 * 2 * 5
